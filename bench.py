@@ -1,0 +1,226 @@
+#!/usr/bin/env python3
+"""Rollout throughput benchmark on one MI355X.
+
+One step = one prefill over every corpus sequence of the workload (the shared
+prefix key/value cache and features) plus the greedy rollout of every anchor
+(block slots each: tokens, full-vocabulary log-probs, features).  Inputs are
+resident in HBM before the timed region starts.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def site_work(site: str, w) -> dict:
+    """Algorithmic FLOPs (or bytes) of one launch at a profiled site."""
+    s = w.shape
+    d, F, V = s.d_model, s.d_ffn, s.vocab
+    qd, kvd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+    T, NA = w.n_tokens, w.n_anchors
+    gemm = {"prefill_qkv": (T, qd + 2 * kvd, d), "prefill_o": (T, d, qd),
+            "prefill_gu": (T, 2 * F, d), "prefill_down": (T, d, F),
+            "decode_qkv": (NA, qd + 2 * kvd, d), "decode_o": (NA, d, qd),
+            "decode_gu": (NA, 2 * F, d), "decode_down": (NA, d, F), "lm_gemm": (NA, V, d)}
+    if site in gemm:
+        m, n, k = gemm[site]
+        return {"bound": "mfma", "flops": 2.0 * m * n * k, "unit": "TFLOP/s"}
+    if site == "lm_finalize":
+        # one fp32 read (max/argmax/sum-exp pass) and one read+write (log-softmax) per entry
+        return {"bound": "hbm", "bytes": 12.0 * NA * V, "unit": "GB/s"}
+    if site == "prefill_attn":
+        # causal: sum over positions of 4 * hd * (t+1) per head
+        L = w.seq_len
+        return {"bound": "mfma", "flops": 4.0 * s.head_dim * s.n_heads * w.n_seq * L * (L + 1) / 2,
+                "unit": "TFLOP/s"}
+    raise KeyError(site)
+
+
+def cpu_baseline(inp, budget_layers=(1, 2)):
+    """Time the oracle (teacher-forced, fp64) on one anchor with the model truncated to
+    1 and 2 decoder layers; extrapolate linearly in depth to the full model."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2609_38795_amd import workloads as W
+
+    w = inp.workload
+    i = int(np.argmin(inp.anchor_pos))  # the anchor with the shortest prefix
+    a_seq, a_pos = inp.anchor_seq[i:i + 1], inp.anchor_pos[i:i + 1]
+    feed = np.zeros((1, w.block), np.int64)
+    rows = mask = None
+    if inp.embeds is not None:
+        rows = inp.embeds.reshape(w.n_seq, w.seq_len, -1)
+        mask = inp.embed_mask.reshape(w.n_seq, w.seq_len)
+    times = {}
+    for nl in budget_layers:
+        shape = W.scaled(w, "trunc", n_layers=nl, feat_layers=tuple(range(min(nl, 1)))).shape
+        wt = dict(inp.weights)
+        wt["layers"] = inp.weights["layers"][:nl]
+        P = O.Params(wt, cache=False)
+        t0 = time.perf_counter()
+        O.rollout_teacher_forced(P, shape, inp.tokens, a_seq, a_pos, w.block, feed,
+                                 given_rows=rows, given_mask=mask,
+                                 emulate_bf16=(w.shape.dtype == "bf16"))
+        times[nl] = time.perf_counter() - t0
+    l1, l2 = budget_layers
+    per_layer = (times[l2] - times[l1]) / (l2 - l1)
+    fixed = times[l1] - l1 * per_layer
+    t_full = fixed + w.shape.n_layers * per_layer
+    try:
+        from threadpoolctl import threadpool_info
+
+        cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) or 1
+    except Exception:
+        cores = os.cpu_count() or 1
+    return {"value": w.block / t_full, "unit": "rollout slots/s", "cores": cores, "kind": "oracle",
+            "sample": (f"fp64 teacher-forced oracle, 1 anchor (position {int(a_pos[0])}, "
+                       f"{w.block} slots) with the model cut to {l1} and {l2} decoder layers "
+                       f"({times[l1]:.1f} s, {times[l2]:.1f} s), extrapolated linearly to "
+                       f"{w.shape.n_layers} layers ({t_full:.1f} s per anchor)")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="llama8b_like")
+    ap.add_argument("--site", default="prefill_gu", help="kernel launch site for the roofline")
+    ap.add_argument("--breakdown", action="store_true", help="time every launch site (extra steps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(multi-GPU sharding by sequence is a design note, not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_38795_amd import binding, workloads as W
+
+    w = W.get(args.workload)
+    t0 = time.time()
+    inp = W.make_inputs(w, progress=lambda m: log(f"[bench] {m} ({time.time() - t0:.0f}s)"))
+    log(f"[bench] {w.name}: inputs drawn in {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    lim = binding.make_limits(w.n_tokens, w.n_seq, w.n_anchors, w.block)
+    t0 = time.time()
+    eng = binding.Engine(w.shape, inp.weights, w.max_pos, lim, device=dev)
+    torch.cuda.synchronize()
+    log(f"[bench] context created ({eng.ws_bytes / 2**30:.1f} GiB workspace) in {time.time() - t0:.1f}s")
+    toks = torch.from_numpy(inp.tokens.reshape(-1).astype(np.int32)).to(dev)
+    emb = mask = None
+    if inp.embeds is not None:
+        e = inp.embeds
+        emb = torch.from_numpy(e.view(np.int16) if e.dtype == np.uint16 else e).to(dev)
+        mask = torch.from_numpy(inp.embed_mask).to(dev)
+    outs = eng.alloc_outputs(w.n_anchors, w.block, want_feats=True)
+    seq_lens = [w.seq_len] * w.n_seq
+    stream = eng.stream
+
+    def step():
+        eng.prefill(toks, seq_lens, emb, mask)
+        eng.rollout(inp.anchor_seq, inp.anchor_pos, w.block, out=outs)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup step {i + 1}/{args.warmup} done")
+
+    # phase split (untimed): prefill vs rollout
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0.record(stream)
+    eng.prefill(toks, seq_lens, emb, mask)
+    e1.record(stream)
+    eng.rollout(inp.anchor_seq, inp.anchor_pos, w.block, out=outs)
+    e2.record(stream)
+    torch.cuda.synchronize()
+    prefill_ms, rollout_ms = e0.elapsed_time(e1), e1.elapsed_time(e2)
+    log(f"[bench] phases: prefill {prefill_ms:.1f} ms, rollout {rollout_ms:.1f} ms")
+
+    breakdown = {}
+    if args.breakdown:
+        for site in binding.PROF_SITES:
+            binding.profile_start(eng, site, 8192)
+            step()
+            ms, n = binding.profile_stop(eng)
+            breakdown[site] = {"ms_per_step": round(ms, 3), "launches": n}
+            log(f"[bench] {site}: {ms:.2f} ms over {n} launches")
+
+    # timed region: exactly K steps, synchronised on both sides
+    binding.profile_start(eng, args.site, 8192)
+    torch.cuda.synchronize()
+    ev_a, ev_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start = time.perf_counter()
+    ev_a.record(stream)
+    for i in range(args.steps):
+        step()
+    ev_b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    site_ms, site_n = binding.profile_stop(eng)
+    ms_per_step = max(wall * 1e3, ev_a.elapsed_time(ev_b)) / args.steps
+    slots = w.n_anchors * w.block
+    value = slots / (ms_per_step / 1e3)
+    log(f"[bench] {args.steps} steps: {ms_per_step:.1f} ms/step, {value:.0f} slots/s")
+
+    work = site_work(args.site, w)
+    avg_s = site_ms / max(site_n, 1) / 1e3
+    if work["bound"] == "mfma":
+        achieved = work["flops"] / avg_s / 1e12
+        peak = PEAK_BF16_TFLOPS if w.shape.dtype == "bf16" else PEAK_F32_TFLOPS
+    else:
+        achieved = work["bytes"] / avg_s / 1e9
+        peak = PEAK_HBM_GBS
+    roofline = {"bound": work["bound"], "achieved": round(achieved, 2), "peak": peak,
+                "unit": work["unit"], "frac": round(achieved / peak, 4), "traffic": None,
+                "kernel": args.site, "avg_launch_ms": round(avg_s * 1e3, 4),
+                "launches_timed": site_n}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        cpu = cpu_baseline(inp)
+        log(f"[bench] cpu baseline: {cpu['value']:.4f} slots/s ({time.time() - t0:.1f}s)")
+
+    line = {
+        "metric": "rollout slots/sec (anchors x block) at 8B-like shapes; MFMA % and HBM GB/s",
+        "value": round(value, 1), "unit": "slots/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.shape.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random weights and Zipf tokens)",
+        "config": {"workload": w.name, "desc": w.description, "n_seq": w.n_seq,
+                   "seq_len": w.seq_len, "anchors": w.n_anchors, "block": w.block,
+                   "slots_per_step": slots},
+        "phases_ms": {"prefill": round(prefill_ms, 2), "rollout": round(rollout_ms, 2),
+                      "rollout_only_slots_per_s": round(slots / (rollout_ms / 1e3), 1)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    if breakdown:
+        line["breakdown_ms_per_step"] = breakdown
+    print(json.dumps(line), flush=True)
+    eng.close()
+
+
+if __name__ == "__main__":
+    main()

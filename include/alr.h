@@ -1,0 +1,189 @@
+/*
+ * alr.h -- C ABI of the anchor-branched greedy-rollout library (gfx950 / MI355X).
+ *
+ * The library computes, for a fixed corpus and a set of anchor positions, the
+ * target model's greedy continuation of every anchor's prefix, one draft block
+ * long: Eq. 3 of Sec. 3.2 ("Labels from the target's rollout").  Following the
+ * "Rollout implementation" paragraph of App. A ("Training Configuration"), one
+ * forward pass over each corpus sequence (alr_prefill) fills a key/value cache
+ * that all of that sequence's anchors share; each rollout step (alr_rollout)
+ * then runs every anchor's newest token through the decoder as one batch, the
+ * query of an anchor attending under one softmax to the cached corpus keys up
+ * to its anchor and to its own rollout keys, kept in a separate per-anchor
+ * buffer; labels are read from the final normalised hidden state through the
+ * output head, greedy ties go to the lower token id, and the residual-stream
+ * outputs of chosen layers are stored as features.
+ *
+ * Slot convention.  Slot s (0 <= s < block) of anchor a sits at position a+s.
+ * Its input token is the corpus token x_a for s = 0 and the token fed after
+ * slot s-1 otherwise.  It outputs log p(. | x_{<=a}, y_1..y_s) over the whole
+ * vocabulary (the paper's label for draft slot k = s+1), its greedy token
+ * y_{s+1}, and the outputs of the feature layers at position a+s.
+ *
+ * Model.  Llama-style decoder: per layer h += Wo Attn(RoPE(Wq n1), RoPE(Wk n1),
+ * Wv n1) with n1 = RMSNorm(h), then h += Wd (SiLU(Wg n2) * Wu n2) with
+ * n2 = RMSNorm(h); RMSNorm(x) = x g / sqrt(mean(x^2) + eps); grouped-query
+ * attention maps query head j to key/value head j / (n_heads/n_kv_heads);
+ * scores are scaled by 1/sqrt(head_dim); RoPE rotates the pairs
+ * (i, i + head_dim/2) by pos * rope_base^(-2i/head_dim).
+ *
+ * Precision.  ALR_F32: all storage and arithmetic in fp32.  ALR_BF16: weights
+ * and GEMM operands (RMSNorm outputs, q/k after RoPE, v, attention output,
+ * SwiGLU output) are bf16; accumulation, residual stream, softmax statistics
+ * and logits are fp32.  Log-probabilities and features are always returned in
+ * fp32.
+ *
+ * Memory and ownership.  All device memory is owned by the caller: weights,
+ * inputs, outputs and one workspace whose size alr_workspace_bytes() gives.
+ * The library allocates no device memory.  alr_create copies (repacks) the
+ * weights into the workspace, so the weight buffers may be freed after it
+ * returns.  The shared key/value cache lives in the workspace and stays valid
+ * until the next alr_prefill on the same context.
+ *
+ * Execution.  Every compute call only enqueues work on the given stream and
+ * returns; results are valid once the stream has been synchronised.  A context
+ * is not thread-safe: use one context per host thread and stream.  Errors are
+ * reported through the return code; nothing is thrown across the ABI.  All
+ * argument checks happen on the host before anything is enqueued, so a call
+ * that returns an error has launched nothing.  alr_last_error() gives a
+ * message for the last failing call on a context.
+ */
+#ifndef ALR_H
+#define ALR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ALR_OK = 0,
+  ALR_E_INVALID_ARG = 1,  /* null pointer, non-positive count, bad config field  */
+  ALR_E_OUT_OF_RANGE = 2, /* anchor, sequence, token or position outside bounds  */
+  ALR_E_WORKSPACE = 3,    /* workspace smaller than alr_workspace_bytes() says   */
+  ALR_E_STATE = 4,        /* rollout before any prefill                           */
+  ALR_E_UNSUPPORTED = 5,  /* shape the kernels do not handle (see alr_config)     */
+  ALR_E_HIP = 6           /* HIP runtime error; alr_last_error() has its text     */
+} alr_status;
+
+typedef enum { ALR_F32 = 0, ALR_BF16 = 1 } alr_dtype;
+
+#define ALR_MAX_FEAT 8
+
+/* Model shape.  Requirements checked by every entry point:
+ *   n_layers >= 0; d_model, d_ffn, n_heads*head_dim and n_kv_heads*head_dim are
+ *   multiples of 64; head_dim is even and <= 256; n_heads % n_kv_heads == 0;
+ *   (n_heads*head_dim/2) and (n_kv_heads*head_dim/2) are multiples of 32;
+ *   vocab is a multiple of 64; 0 <= feat_layers[i] < n_layers;
+ *   max_pos >= 1 bounds every position a slot may reach (a + block - 1). */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  float rms_eps, rope_base;
+  int32_t dtype;   /* alr_dtype */
+  int32_t max_pos;
+  int32_t n_feat;  /* 0 .. ALR_MAX_FEAT */
+  int32_t feat_layers[ALR_MAX_FEAT];
+} alr_config;
+
+/* Device pointers to the weights, element type given by alr_config.dtype
+ * (float for ALR_F32, bf16 bit patterns for ALR_BF16), row-major, [out, in]
+ * layout of a linear map y = W x.  The per-layer fields are HOST arrays of
+ * n_layers DEVICE pointers.  Shapes: tok_embed and lm_head [vocab, d_model];
+ * final_norm, attn_norm[l], ffn_norm[l] [d_model]; wq [n_heads*head_dim,
+ * d_model]; wk, wv [n_kv_heads*head_dim, d_model]; wo [d_model,
+ * n_heads*head_dim]; w_gate, w_up [d_ffn, d_model]; w_down [d_model, d_ffn]. */
+typedef struct {
+  const void* tok_embed;
+  const void* final_norm;
+  const void* lm_head;
+  const void* const* attn_norm;
+  const void* const* wq;
+  const void* const* wk;
+  const void* const* wv;
+  const void* const* wo;
+  const void* const* ffn_norm;
+  const void* const* w_gate;
+  const void* const* w_up;
+  const void* const* w_down;
+} alr_weights;
+
+typedef struct alr_ctx alr_ctx;
+typedef void* alr_stream; /* a hipStream_t; NULL is the null stream */
+
+/* Capacity limits a context is created for. */
+typedef struct {
+  int32_t max_tokens;  /* total corpus tokens over all sequences of one prefill */
+  int32_t max_seqs;    /* sequences per prefill                                 */
+  int32_t max_anchors; /* anchors per rollout                                    */
+  int32_t max_block;   /* slots per anchor (block)                               */
+} alr_limits;
+
+/* Bytes of device workspace a context with this config and these limits needs.
+ * Returns 0 if the config or limits are invalid.  Host only, no GPU needed. */
+size_t alr_workspace_bytes(const alr_config* cfg, const alr_limits* lim);
+
+/* Validate cfg (host only, no GPU needed).  On failure writes a message into
+ * msg (if msg_len > 0) and returns the status alr_create would return. */
+alr_status alr_check_config(const alr_config* cfg, char* msg, size_t msg_len);
+
+/* Validate a rollout request against a prefill of n_seq sequences of lengths
+ * seq_len[] (host arrays) and the limits (host only, no GPU needed).  Same
+ * checks and status codes as alr_rollout. */
+alr_status alr_check_rollout(const alr_config* cfg, const alr_limits* lim, int32_t n_seq,
+                             const int32_t* seq_len, int32_t n_anchor,
+                             const int32_t* anchor_seq, const int32_t* anchor_pos,
+                             int32_t block, char* msg, size_t msg_len);
+
+/* Create a context.  workspace: device buffer of ws_bytes >= alr_workspace_bytes
+ * (256-byte aligned); the weights are repacked into it on `stream`.  On success
+ * *out receives the context.  Synchronises `stream` before returning. */
+alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_limits* lim,
+                      void* workspace, size_t ws_bytes, alr_stream stream, alr_ctx** out);
+
+/* Forward pass over n_seq corpus sequences (the shared prefix of every anchor).
+ *   seq_len    HOST [n_seq], each >= 1 and <= max_pos; sum <= max_tokens.
+ *   tokens     DEVICE int32 [sum seq_len], sequences concatenated; ids < vocab.
+ *   embeds     DEVICE [sum seq_len, d_model] in the weight dtype, or NULL: rows
+ *              used instead of the token embedding where embed_mask is nonzero.
+ *   embed_mask DEVICE uint8 [sum seq_len], or NULL (both or neither).
+ *   feats_out  DEVICE fp32 [sum seq_len, n_feat, d_model] or NULL: residual
+ *              stream after each feature layer at every corpus position.
+ * Token ids are not range-checked on the device: ids outside [0, vocab) give
+ * undefined results, so the caller must validate them. */
+alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len,
+                       const int32_t* tokens, const void* embeds,
+                       const uint8_t* embed_mask, float* feats_out, alr_stream stream);
+
+/* Greedy rollout of `block` slots from every anchor of the last prefill.
+ *   anchor_seq, anchor_pos  HOST int32 [n_anchor]: sequence index and position;
+ *              0 <= anchor_pos < seq_len[anchor_seq]; anchor_pos + block - 1 <
+ *              max_pos.  Any order; duplicates allowed (identical outputs).
+ *   forced     DEVICE int32 [n_anchor, block] or NULL: where forced[i,s] >= 0 it
+ *              is fed to slot s+1 instead of the greedy token (column block-1
+ *              is ignored); values must be < vocab.
+ *   tokens_out DEVICE int32 [n_anchor, block]: greedy token of every slot.
+ *   logprobs_out DEVICE fp32 [n_anchor, block, vocab]: log-softmax of each slot.
+ *   feats_out  DEVICE fp32 [n_anchor, block, n_feat, d_model] or NULL.
+ * Outputs are in the caller's anchor order. */
+alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                       const int32_t* anchor_pos, int32_t block, const int32_t* forced,
+                       int32_t* tokens_out, float* logprobs_out, float* feats_out,
+                       alr_stream stream);
+
+/* Message of the last failing call on ctx ("" if none); ctx may be NULL, then
+ * the message of the last failing alr_create in this thread is returned. */
+const char* alr_last_error(const alr_ctx* ctx);
+
+/* Static name of a status code. */
+const char* alr_status_string(alr_status st);
+
+/* Destroy a context (host memory only; the workspace stays the caller's). */
+void alr_destroy(alr_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALR_H */

@@ -1,0 +1,56 @@
+/*
+ * alr_debug.h -- kernel-level test hooks of the rollout library.
+ *
+ * These entry points expose single kernels of the library so that tests can
+ * check them in isolation and benchmarks can time them.  They are not needed
+ * to run the rollout.
+ */
+#ifndef ALR_DEBUG_H
+#define ALR_DEBUG_H
+
+#include <stdint.h>
+
+#include "alr.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* C[M,N] (fp32, row-major) = A[M,K] * W[N,K]^T, on the library's GEMM kernel
+ * for `dtype` (ALR_BF16: bf16 MFMA with fp32 accumulation; ALR_F32: fp32 FMA).
+ * All pointers are device pointers, row-major and contiguous; N and K must be
+ * multiples of 64 (ALR_E_UNSUPPORTED otherwise).  Enqueued on `stream`. */
+alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
+                          int32_t N, int32_t K, alr_stream stream);
+
+/* Kernel launch sites whose device time can be measured with alr_profile_*. */
+typedef enum {
+  ALR_PROF_PREFILL_QKV = 1,   /* prefill QKV GEMM (+RoPE, shared K/V store)        */
+  ALR_PROF_PREFILL_ATTN = 2,  /* prefill causal attention                           */
+  ALR_PROF_PREFILL_O = 3,     /* prefill attention-output GEMM (+residual)          */
+  ALR_PROF_PREFILL_GU = 4,    /* prefill gate|up GEMM (+SwiGLU)                     */
+  ALR_PROF_PREFILL_DOWN = 5,  /* prefill down GEMM (+residual, features)            */
+  ALR_PROF_DECODE_QKV = 6,    /* rollout-step QKV GEMM (+RoPE, private K/V append)  */
+  ALR_PROF_DECODE_ATTN = 7,   /* rollout-step anchor-branched attention             */
+  ALR_PROF_DECODE_O = 8,
+  ALR_PROF_DECODE_GU = 9,
+  ALR_PROF_DECODE_DOWN = 10,
+  ALR_PROF_LM_GEMM = 11,      /* output-head GEMM (logits into the caller's rows)   */
+  ALR_PROF_LM_FINALIZE = 12,  /* log-sum-exp, greedy argmax, in-place log-softmax   */
+  ALR_PROF_COUNT = 13
+} alr_prof_site;
+
+/* Start timing every launch at `site` with HIP events recorded on the launch
+ * stream, for up to `capacity` launches (later launches are not timed).
+ * Creates 2*capacity events (host-side HIP objects, no device buffers). */
+alr_status alr_profile_start(alr_ctx* ctx, int32_t site, int32_t capacity);
+
+/* Stop timing; waits for the last recorded event and returns the summed
+ * device time (ms) and the number of timed launches.  Destroys the events. */
+alr_status alr_profile_stop(alr_ctx* ctx, double* total_ms, int32_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALR_DEBUG_H */

@@ -1,0 +1,291 @@
+"""Thin ctypes binding of libalr.so (argument marshalling only).
+
+Every step of the rollout runs in the library's HIP kernels; this module only
+turns Python/torch objects into the C ABI's plain pointers and sizes.  PyTorch
+provides device memory and streams.  If the library is missing the binding
+raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libalr.so")
+
+ALR_F32, ALR_BF16 = 0, 1
+ALR_MAX_FEAT = 8
+STATUS = {0: "ALR_OK", 1: "ALR_E_INVALID_ARG", 2: "ALR_E_OUT_OF_RANGE", 3: "ALR_E_WORKSPACE",
+          4: "ALR_E_STATE", 5: "ALR_E_UNSUPPORTED", 6: "ALR_E_HIP"}
+
+# Every function the C headers declare (include/alr.h, include/alr_debug.h).
+EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_create",
+           "alr_prefill", "alr_rollout", "alr_last_error", "alr_status_string", "alr_destroy",
+           "alr_debug_gemm", "alr_profile_start", "alr_profile_stop")
+
+
+class AlrConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
+                ("max_pos", ctypes.c_int32), ("n_feat", ctypes.c_int32),
+                ("feat_layers", ctypes.c_int32 * ALR_MAX_FEAT)]
+
+
+class AlrLimits(ctypes.Structure):
+    _fields_ = [("max_tokens", ctypes.c_int32), ("max_seqs", ctypes.c_int32),
+                ("max_anchors", ctypes.c_int32), ("max_block", ctypes.c_int32)]
+
+
+_PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+class AlrWeights(ctypes.Structure):
+    _fields_ = [("tok_embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("lm_head", ctypes.c_void_p), ("attn_norm", _PP), ("wq", _PP), ("wk", _PP),
+                ("wv", _PP), ("wo", _PP), ("ffn_norm", _PP), ("w_gate", _PP), ("w_up", _PP),
+                ("w_down", _PP)]
+
+
+class AlrError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load_library() -> ctypes.CDLL:
+    """Load libalr.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(the rollout has no non-HIP path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, vp, sz = ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t
+    cfgp, limp = ctypes.POINTER(AlrConfig), ctypes.POINTER(AlrLimits)
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.alr_workspace_bytes.argtypes = [cfgp, limp]
+    lib.alr_workspace_bytes.restype = sz
+    lib.alr_check_config.argtypes = [cfgp, ctypes.c_char_p, sz]
+    lib.alr_check_config.restype = ctypes.c_int
+    lib.alr_check_rollout.argtypes = [cfgp, limp, i32, i32p, i32, i32p, i32p, i32,
+                                      ctypes.c_char_p, sz]
+    lib.alr_check_rollout.restype = ctypes.c_int
+    lib.alr_create.argtypes = [cfgp, ctypes.POINTER(AlrWeights), limp, vp, sz, vp,
+                               ctypes.POINTER(vp)]
+    lib.alr_create.restype = ctypes.c_int
+    lib.alr_prefill.argtypes = [vp, i32, i32p, vp, vp, vp, vp, vp]
+    lib.alr_prefill.restype = ctypes.c_int
+    lib.alr_rollout.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp]
+    lib.alr_rollout.restype = ctypes.c_int
+    lib.alr_last_error.argtypes = [vp]
+    lib.alr_last_error.restype = ctypes.c_char_p
+    lib.alr_status_string.argtypes = [ctypes.c_int]
+    lib.alr_status_string.restype = ctypes.c_char_p
+    lib.alr_destroy.argtypes = [vp]
+    lib.alr_destroy.restype = None
+    lib.alr_debug_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, vp]
+    lib.alr_debug_gemm.restype = ctypes.c_int
+    lib.alr_profile_start.argtypes = [vp, i32, i32]
+    lib.alr_profile_start.restype = ctypes.c_int
+    lib.alr_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
+    lib.alr_profile_stop.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def make_config(shape, max_pos: int) -> AlrConfig:
+    c = AlrConfig()
+    c.n_layers, c.d_model, c.n_heads = shape.n_layers, shape.d_model, shape.n_heads
+    c.n_kv_heads, c.head_dim, c.d_ffn, c.vocab = (shape.n_kv_heads, shape.head_dim, shape.d_ffn,
+                                                   shape.vocab)
+    c.rms_eps, c.rope_base = shape.rms_eps, shape.rope_base
+    c.dtype = ALR_BF16 if shape.dtype == "bf16" else ALR_F32
+    c.max_pos = max_pos
+    c.n_feat = len(shape.feat_layers)
+    for i, f in enumerate(shape.feat_layers):
+        c.feat_layers[i] = f
+    return c
+
+
+def make_limits(max_tokens: int, max_seqs: int, max_anchors: int, max_block: int) -> AlrLimits:
+    lim = AlrLimits()
+    lim.max_tokens, lim.max_seqs, lim.max_anchors, lim.max_block = (max_tokens, max_seqs,
+                                                                    max_anchors, max_block)
+    return lim
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def check_rollout(shape, max_pos, limits: AlrLimits, seq_len: Sequence[int], anchor_seq,
+                  anchor_pos, block: int):
+    """Host-only validation of a rollout request (no GPU needed): (status, message)."""
+    lib = load_library()
+    cfg = make_config(shape, max_pos)
+    sl = np.ascontiguousarray(seq_len, dtype=np.int32)
+    a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+    a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+    buf = ctypes.create_string_buffer(256)
+    st = lib.alr_check_rollout(ctypes.byref(cfg), ctypes.byref(limits), len(sl), _i32p(sl),
+                               len(a_s), _i32p(a_s), _i32p(a_p), block, buf, 256)
+    return st, buf.value.decode()
+
+
+class Engine:
+    """One library context: weights repacked into a caller-owned workspace.
+
+    ``weights`` is the generator's dict (numpy float32 or uint16 bf16 bits);
+    they are uploaded, repacked by the library and released again.
+    """
+
+    def __init__(self, shape, weights: Dict, max_pos: int, limits: AlrLimits, device="cuda",
+                 stream=None):
+        import torch
+
+        self.torch = torch
+        self.lib = load_library()
+        self.shape = shape
+        self.device = torch.device(device)
+        self.cfg = make_config(shape, max_pos)
+        self.limits = limits
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = self.lib.alr_workspace_bytes(ctypes.byref(self.cfg), ctypes.byref(limits))
+        if nbytes == 0:
+            buf = ctypes.create_string_buffer(256)
+            st = self.lib.alr_check_config(ctypes.byref(self.cfg), buf, 256)
+            raise AlrError(st or 1, buf.value.decode() or "invalid limits")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.ws_bytes = nbytes
+        dev_w = self._upload_weights(weights)
+        w = AlrWeights()
+        keep = []
+
+        def arr(name):
+            a = (ctypes.c_void_p * max(1, shape.n_layers))(
+                *[dev_w["layers"][l][name].data_ptr() for l in range(shape.n_layers)])
+            keep.append(a)
+            return ctypes.cast(a, _PP)
+
+        w.tok_embed = dev_w["tok_embed"].data_ptr()
+        w.final_norm = dev_w["final_norm"].data_ptr()
+        w.lm_head = dev_w["lm_head"].data_ptr()
+        for n in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down"):
+            setattr(w, n, arr(n))
+        ctx = ctypes.c_void_p()
+        st = self.lib.alr_create(ctypes.byref(self.cfg), ctypes.byref(w), ctypes.byref(limits),
+                                 self.workspace.data_ptr(), nbytes, self._sp(), ctypes.byref(ctx))
+        if st != 0:
+            raise AlrError(st, self.lib.alr_last_error(None).decode())
+        self.ctx = ctx
+        del dev_w, keep
+
+    def _sp(self):
+        return ctypes.c_void_p(self.stream.cuda_stream)
+
+    def _to_dev(self, a: np.ndarray):
+        torch = self.torch
+        if a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(self.device)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.device)
+
+    def _upload_weights(self, w: Dict) -> Dict:
+        out = {k: self._to_dev(w[k]) for k in ("tok_embed", "final_norm", "lm_head")}
+        out["layers"] = [{k: self._to_dev(v) for k, v in ld.items()} for ld in w["layers"]]
+        return out
+
+    def _err(self, st: int):
+        raise AlrError(st, self.lib.alr_last_error(self.ctx).decode())
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.lib.alr_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- calls
+    def prefill(self, tokens, seq_len: Sequence[int], embeds=None, embed_mask=None,
+                feats_out=None):
+        """tokens: device int32 tensor [sum seq_len]; embeds/embed_mask device tensors or None."""
+        sl = np.ascontiguousarray(seq_len, dtype=np.int32)
+        self._seq_len = sl
+        st = self.lib.alr_prefill(self.ctx, len(sl), _i32p(sl), tokens.data_ptr(),
+                                  None if embeds is None else embeds.data_ptr(),
+                                  None if embed_mask is None else embed_mask.data_ptr(),
+                                  None if feats_out is None else feats_out.data_ptr(), self._sp())
+        if st != 0:
+            self._err(st)
+
+    def alloc_outputs(self, n_anchor: int, block: int, want_feats: bool = True):
+        torch = self.torch
+        tok = torch.empty((n_anchor, block), dtype=torch.int32, device=self.device)
+        lp = torch.empty((n_anchor, block, self.shape.vocab), dtype=torch.float32,
+                         device=self.device)
+        ft = None
+        if want_feats and self.shape.n_feat > 0:
+            ft = torch.empty((n_anchor, block, self.shape.n_feat, self.shape.d_model),
+                             dtype=torch.float32, device=self.device)
+        return tok, lp, ft
+
+    def rollout(self, anchor_seq, anchor_pos, block: int, forced=None, out=None,
+                want_feats: bool = True):
+        a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+        a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+        n = len(a_s)
+        tok, lp, ft = out if out is not None else self.alloc_outputs(n, block, want_feats)
+        st = self.lib.alr_rollout(self.ctx, n, _i32p(a_s), _i32p(a_p), block,
+                                  None if forced is None else forced.data_ptr(), tok.data_ptr(),
+                                  lp.data_ptr(), None if ft is None else ft.data_ptr(), self._sp())
+        if st != 0:
+            self._err(st)
+        return tok, lp, ft
+
+
+PROF_SITES = {"prefill_qkv": 1, "prefill_attn": 2, "prefill_o": 3, "prefill_gu": 4,
+              "prefill_down": 5, "decode_qkv": 6, "decode_attn": 7, "decode_o": 8, "decode_gu": 9,
+              "decode_down": 10, "lm_gemm": 11, "lm_finalize": 12}
+
+
+def profile_start(eng: "Engine", site: str, capacity: int = 4096):
+    st = eng.lib.alr_profile_start(eng.ctx, PROF_SITES[site], capacity)
+    if st != 0:
+        eng._err(st)
+
+
+def profile_stop(eng: "Engine"):
+    """-> (total device ms, number of timed launches)"""
+    ms = ctypes.c_double()
+    n = ctypes.c_int32()
+    st = eng.lib.alr_profile_stop(eng.ctx, ctypes.byref(ms), ctypes.byref(n))
+    if st != 0:
+        eng._err(st)
+    return ms.value, n.value
+
+
+def debug_gemm(dtype: int, A, W, C, stream=None):
+    """C = A W^T on the library's GEMM kernel (device tensors, fp32 C)."""
+    import torch
+
+    lib = load_library()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    M, K = A.shape
+    N = W.shape[0]
+    st = lib.alr_debug_gemm(dtype, A.data_ptr(), W.data_ptr(), C.data_ptr(), M, N, K,
+                            ctypes.c_void_p(s.cuda_stream))
+    if st != 0:
+        raise AlrError(st, "alr_debug_gemm")

@@ -1,0 +1,890 @@
+// Host runtime and C ABI of the anchor-branched greedy-rollout library.
+//
+// Call sequence per prefill (all sequences of the batch at once, M = total
+// tokens): embed -> per layer [RMSNorm -> QKV GEMM (+RoPE, shared K/V store)
+// -> causal attention -> O GEMM (+residual) -> RMSNorm -> gate|up GEMM
+// (+SwiGLU) -> down GEMM (+residual, feature capture)] -> final RMSNorm.
+//
+// Call sequence per rollout: anchors are sorted by (sequence, position) so the
+// decode attention can stream each sequence's shared keys once per group of
+// anchors; slot 0 reads the prefill's final-norm row and features at the
+// anchor; each later slot runs all anchors through the decoder as one batch
+// (M = number of anchors), appending its key/value to the anchor's private
+// buffer, and ends with the output-head GEMM and its finalisation.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <type_traits>
+#include <vector>
+
+#include "../../include/alr.h"
+#include "../../include/alr_debug.h"
+#include "attn_kernels.hpp"
+#include "gemm_kernels.hpp"
+#include "misc_kernels.hpp"
+
+using namespace alr;
+
+namespace {
+
+thread_local std::string g_create_err;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+  size_t es;  // element size of the weight / operand dtype
+  size_t w_embed, w_lm, w_fnorm;
+  size_t layer0, layer_stride;  // per layer block
+  size_t l_anorm, l_fnorm, l_qkv, l_o, l_gu, l_down;  // offsets within a layer block
+  size_t rope_cos, rope_sin;
+  size_t kc, vc, kv_layer_stride;
+  size_t kp, vp, kvp_layer_stride;
+  size_t feat_store, hf_store;
+  size_t resid, xnorm, qbuf, attn, act;
+  size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_cur;
+  size_t i_pwork, i_dwork, i_maps;
+  size_t max_pwork, max_dwork;
+  size_t total;
+};
+
+bool fmt_msg(char* msg, size_t len, const char* f, ...) {
+  if (msg && len) {
+    va_list ap;
+    va_start(ap, f);
+    vsnprintf(msg, len, f, ap);
+    va_end(ap);
+  }
+  return false;
+}
+
+alr_status check_config_impl(const alr_config* c, char* msg, size_t len) {
+  if (!c) return fmt_msg(msg, len, "config is NULL"), ALR_E_INVALID_ARG;
+  if (c->dtype != ALR_F32 && c->dtype != ALR_BF16)
+    return fmt_msg(msg, len, "dtype %d is not ALR_F32 or ALR_BF16", c->dtype), ALR_E_INVALID_ARG;
+  if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->d_ffn <= 0 || c->vocab <= 0 || c->max_pos <= 0)
+    return fmt_msg(msg, len, "non-positive dimension in config"), ALR_E_INVALID_ARG;
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f))
+    return fmt_msg(msg, len, "rms_eps must be >= 0 and rope_base > 0"), ALR_E_INVALID_ARG;
+  if (c->n_heads % c->n_kv_heads != 0)
+    return fmt_msg(msg, len, "n_heads %d is not a multiple of n_kv_heads %d", c->n_heads,
+                   c->n_kv_heads),
+           ALR_E_INVALID_ARG;
+  const long q = (long)c->n_heads * c->head_dim, kv = (long)c->n_kv_heads * c->head_dim;
+  if (c->d_model % 64 || c->d_ffn % 64 || q % 64 || kv % 64 || c->vocab % 64)
+    return fmt_msg(msg, len,
+                   "d_model, d_ffn, vocab, n_heads*head_dim and n_kv_heads*head_dim must be "
+                   "multiples of 64"),
+           ALR_E_UNSUPPORTED;
+  if (c->head_dim % 2 || c->head_dim > 256 || (q / 2) % 32 || (kv / 2) % 32)
+    return fmt_msg(msg, len,
+                   "head_dim must be even and <= 256, and heads*head_dim/2 a multiple of 32"),
+           ALR_E_UNSUPPORTED;
+  if (c->n_feat < 0 || c->n_feat > ALR_MAX_FEAT)
+    return fmt_msg(msg, len, "n_feat %d outside [0, %d]", c->n_feat, ALR_MAX_FEAT),
+           ALR_E_INVALID_ARG;
+  for (int i = 0; i < c->n_feat; ++i) {
+    if (c->feat_layers[i] < 0 || c->feat_layers[i] >= c->n_layers)
+      return fmt_msg(msg, len, "feat_layers[%d] = %d outside [0, n_layers)", i, c->feat_layers[i]),
+             ALR_E_OUT_OF_RANGE;
+    for (int j = 0; j < i; ++j)
+      if (c->feat_layers[j] == c->feat_layers[i])
+        return fmt_msg(msg, len, "feat_layers has duplicate layer %d", c->feat_layers[i]),
+               ALR_E_INVALID_ARG;
+  }
+  return ALR_OK;
+}
+
+alr_status check_limits(const alr_limits* l, char* msg, size_t len) {
+  if (!l) return fmt_msg(msg, len, "limits is NULL"), ALR_E_INVALID_ARG;
+  if (l->max_tokens <= 0 || l->max_seqs <= 0 || l->max_anchors <= 0 || l->max_block <= 0)
+    return fmt_msg(msg, len, "limits must be positive"), ALR_E_INVALID_ARG;
+  return ALR_OK;
+}
+
+int anchor_group(const alr_config& c) { return std::max(1, 128 / (c.n_heads / c.n_kv_heads)); }
+
+size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
+  const size_t es = (c.dtype == ALR_BF16) ? 2 : 4;
+  const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, H = c.n_heads, G = c.n_kv_heads,
+               hd = c.head_dim, nl = c.n_layers;
+  const size_t qd = H * hd, kvd = G * hd;
+  const size_t T = lim.max_tokens, NA = lim.max_anchors;
+  const size_t R = std::max(T, NA);
+  const size_t np = lim.max_block > 1 ? (size_t)(lim.max_block - 1) : 0;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  L.es = es;
+  L.w_embed = take(V * d * es);
+  L.w_lm = take(V * d * es);
+  L.w_fnorm = take(d * es);
+  {
+    size_t lo = 0;
+    auto ltake = [&](size_t bytes) {
+      const size_t o = lo;
+      lo = align256(lo + bytes);
+      return o;
+    };
+    L.l_anorm = ltake(d * es);
+    L.l_fnorm = ltake(d * es);
+    L.l_qkv = ltake((qd + 2 * kvd) * d * es);
+    L.l_o = ltake(d * qd * es);
+    L.l_gu = ltake(2 * F * d * es);
+    L.l_down = ltake(d * F * es);
+    L.layer_stride = lo;
+  }
+  L.layer0 = take(nl * L.layer_stride);
+  L.rope_cos = take((size_t)c.max_pos * (hd / 2) * 4);
+  L.rope_sin = take((size_t)c.max_pos * (hd / 2) * 4);
+  L.kv_layer_stride = align256(T * kvd * es);
+  L.kc = take(nl * L.kv_layer_stride);
+  L.vc = take(nl * L.kv_layer_stride);
+  L.kvp_layer_stride = align256(NA * np * kvd * es);
+  L.kp = take(nl * L.kvp_layer_stride);
+  L.vp = take(nl * L.kvp_layer_stride);
+  L.feat_store = take(T * (size_t)c.n_feat * d * 4);
+  L.hf_store = take(T * d * es);
+  L.resid = take(R * d * 4);
+  L.xnorm = take(R * d * es);
+  L.qbuf = take(R * qd * es);
+  L.attn = take(R * qd * es);
+  L.act = take(R * F * es);
+  L.i_tokpos = take(T * 4);
+  L.i_rowstart = take(T * 4);
+  L.i_perm = take(NA * 4);
+  L.i_apos = take(NA * 4);
+  L.i_atok = take(NA * 4);
+  L.i_aseq = take(NA * 4);
+  L.i_cur = take(NA * 4);
+  L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
+  L.max_dwork = (NA + std::min<size_t>(lim.max_seqs, NA)) * G;
+  L.i_pwork = take(L.max_pwork * sizeof(PrefillItem));
+  L.i_dwork = take(L.max_dwork * sizeof(DecodeItem));
+  L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
+  L.total = off;
+  return off;
+}
+
+alr_status check_rollout_impl(const alr_config& c, const alr_limits& lim, int n_seq,
+                              const int32_t* seq_len, int32_t n_anchor, const int32_t* aseq,
+                              const int32_t* apos, int32_t block, char* msg, size_t len) {
+  if (n_anchor <= 0 || n_anchor > lim.max_anchors)
+    return fmt_msg(msg, len, "n_anchor %d outside [1, %d]", n_anchor, lim.max_anchors),
+           ALR_E_INVALID_ARG;
+  if (block <= 0 || block > lim.max_block)
+    return fmt_msg(msg, len, "block %d outside [1, %d]", block, lim.max_block), ALR_E_INVALID_ARG;
+  if (!aseq || !apos || !seq_len)
+    return fmt_msg(msg, len, "anchor arrays must not be NULL"), ALR_E_INVALID_ARG;
+  for (int i = 0; i < n_anchor; ++i) {
+    if (aseq[i] < 0 || aseq[i] >= n_seq)
+      return fmt_msg(msg, len, "anchor %d: sequence %d outside [0, %d)", i, aseq[i], n_seq),
+             ALR_E_OUT_OF_RANGE;
+    if (apos[i] < 0 || apos[i] >= seq_len[aseq[i]])
+      return fmt_msg(msg, len, "anchor %d: position %d outside [0, %d)", i, apos[i],
+                     seq_len[aseq[i]]),
+             ALR_E_OUT_OF_RANGE;
+    if ((long)apos[i] + block - 1 >= c.max_pos)
+      return fmt_msg(msg, len, "anchor %d: last slot position %ld >= max_pos %d", i,
+                     (long)apos[i] + block - 1, c.max_pos),
+             ALR_E_OUT_OF_RANGE;
+  }
+  return ALR_OK;
+}
+
+alr_status check_prefill_impl(const alr_config& c, const alr_limits& lim, int32_t n_seq,
+                              const int32_t* seq_len, const int32_t* tokens, const void* embeds,
+                              const uint8_t* mask, char* msg, size_t len) {
+  if (n_seq <= 0 || n_seq > lim.max_seqs)
+    return fmt_msg(msg, len, "n_seq %d outside [1, %d]", n_seq, lim.max_seqs), ALR_E_INVALID_ARG;
+  if (!seq_len || !tokens) return fmt_msg(msg, len, "seq_len and tokens must not be NULL"), ALR_E_INVALID_ARG;
+  if ((embeds == nullptr) != (mask == nullptr))
+    return fmt_msg(msg, len, "embeds and embed_mask must both be given or both be NULL"),
+           ALR_E_INVALID_ARG;
+  long tot = 0;
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq_len[i] <= 0 || seq_len[i] > c.max_pos)
+      return fmt_msg(msg, len, "seq_len[%d] = %d outside [1, max_pos=%d]", i, seq_len[i], c.max_pos),
+             ALR_E_OUT_OF_RANGE;
+    tot += seq_len[i];
+  }
+  if (tot > lim.max_tokens)
+    return fmt_msg(msg, len, "total tokens %ld > max_tokens %d", tot, lim.max_tokens),
+           ALR_E_OUT_OF_RANGE;
+  return ALR_OK;
+}
+
+}  // namespace
+
+struct alr_ctx {
+  alr_config cfg;
+  alr_limits lim;
+  char* ws;
+  size_t ws_bytes;
+  Layout L;
+  bool prefilled = false;
+  int n_seq = 0;
+  std::vector<int> seq_len, seq_off;
+  std::vector<int> h_tokpos, h_rowstart;
+  std::vector<PrefillItem> h_pwork;
+  std::vector<int> h_anch;  // perm | apos | atok | aseq, each n_anchor long
+  std::vector<DecodeItem> h_dwork;
+  std::string err;
+  // launch timing of one site (alr_profile_*)
+  int prof_site = 0;
+  std::vector<hipEvent_t> prof_ev;
+  size_t prof_used = 0;
+
+  template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
+  char* layer(int l) const { return ws + L.layer0 + (size_t)l * L.layer_stride; }
+};
+
+namespace {
+
+alr_status fail(alr_ctx* ctx, alr_status st, const char* f, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, f);
+  vsnprintf(buf, sizeof(buf), f, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf;
+  else g_create_err = buf;
+  return st;
+}
+
+#define ALR_HIP(ctx, call)                                                                 \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess)                                                                  \
+      return fail(ctx, ALR_E_HIP, "%s failed: %s", #call, hipGetErrorString(e_));          \
+  } while (0)
+
+#define ALR_LAUNCHED(ctx, what)                                                            \
+  do {                                                                                     \
+    hipError_t e_ = hipGetLastError();                                                     \
+    if (e_ != hipSuccess)                                                                  \
+      return fail(ctx, ALR_E_HIP, "launch of %s failed: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+// Event pair around one launch when `site` is the profiled one.
+struct ProfScope {
+  alr_ctx* ctx;
+  hipStream_t st;
+  hipEvent_t end = nullptr;
+  ProfScope(alr_ctx* c, int site, hipStream_t s) : ctx(c), st(s) {
+    if (c->prof_site == site && 2 * (c->prof_used + 1) <= c->prof_ev.size()) {
+      (void)hipEventRecord(c->prof_ev[2 * c->prof_used], s);
+      end = c->prof_ev[2 * c->prof_used + 1];
+      ++c->prof_used;
+    }
+  }
+  ~ProfScope() {
+    if (end) (void)hipEventRecord(end, st);
+  }
+};
+
+template <int TAG, typename T, class Epi>
+void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, int N, int K,
+                 Epi epi, hipStream_t st) {
+  if (M <= 0) return;
+  ProfScope ps(ctx, TAG, st);
+  if constexpr (std::is_same<T, bf16>::value) {
+    const int tm = (M + GB_M - 1) / GB_M, tn = (N + GB_N - 1) / GB_N;
+    gemm_bf16_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+  } else {
+    const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
+    gemm_f32_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+  }
+}
+
+AttnGeom geom(const alr_config& c) {
+  AttnGeom g;
+  g.H = c.n_heads;
+  g.G = c.n_kv_heads;
+  g.hd = c.head_dim;
+  g.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim));
+  return g;
+}
+
+bool mfma_attn(const alr_config& c) {
+  return c.dtype == ALR_BF16 && (c.head_dim == 64 || c.head_dim == 128);
+}
+
+// Column arrangement of the fused QKV weight: for q (n heads of hd), the
+// original row feeding fused row (64 t + w) -- see EpiQKV.
+void rope_pair_rows(int n, int hd, std::vector<int>& dst_of_src) {
+  const int half = hd / 2, tot = n * hd;
+  dst_of_src.assign(tot, -1);
+  for (int nr = 0; nr < tot; ++nr) {
+    const int t = nr / 64, w = nr % 64;
+    const int f = 32 * t + (w & 31);
+    const int head = f / half, i = f % half;
+    const int src = head * hd + i + (w >= 32 ? half : 0);
+    dst_of_src[src] = nr;
+  }
+}
+
+template <typename T>
+alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* feat,
+                         long feat_rs, const int* perm, hipStream_t st) {
+  const alr_config& c = ctx->cfg;
+  const Layout& L = ctx->L;
+  const int d = c.d_model, F = c.d_ffn, H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
+  const int qd = H * hd, kvd = G * hd;
+  char* lw = ctx->layer(l);
+  float* resid = ctx->at<float>(L.resid);
+  T* xn = ctx->at<T>(L.xnorm);
+  T* qb = ctx->at<T>(L.qbuf);
+  T* at = ctx->at<T>(L.attn);
+  T* act = ctx->at<T>(L.act);
+  T* kc = reinterpret_cast<T*>(ctx->ws + L.kc + (size_t)l * L.kv_layer_stride);
+  T* vc = reinterpret_cast<T*>(ctx->ws + L.vc + (size_t)l * L.kv_layer_stride);
+  T* kp = reinterpret_cast<T*>(ctx->ws + L.kp + (size_t)l * L.kvp_layer_stride);
+  T* vp = reinterpret_cast<T*>(ctx->ws + L.vp + (size_t)l * L.kvp_layer_stride);
+  const int np = ctx->lim.max_block - 1;
+  const long priv_rs = (long)np * kvd;
+
+  rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, reinterpret_cast<const T*>(lw + L.l_anorm), xn, d,
+                                       c.rms_eps);
+  EpiQKV<T> eq;
+  eq.q = qb;
+  eq.cosT = ctx->at<float>(L.rope_cos);
+  eq.sinT = ctx->at<float>(L.rope_sin);
+  eq.H = H;
+  eq.G = G;
+  eq.hd = hd;
+  if (!decode) {
+    eq.k = kc;
+    eq.v = vc;
+    eq.kv_rs = kvd;
+    eq.pos = ctx->at<int>(L.i_tokpos);
+    eq.pos_add = 0;
+  } else {
+    eq.k = kp + (long)(s - 1) * kvd;
+    eq.v = vp + (long)(s - 1) * kvd;
+    eq.kv_rs = priv_rs;
+    eq.pos = ctx->at<int>(L.i_apos);
+    eq.pos_add = s;
+  }
+  if (decode)
+    launch_gemm<ALR_PROF_DECODE_QKV, T>(ctx, xn, d, reinterpret_cast<const T*>(lw + L.l_qkv), d, M,
+                                        qd + 2 * kvd, d, eq, st);
+  else
+    launch_gemm<ALR_PROF_PREFILL_QKV, T>(ctx, xn, d, reinterpret_cast<const T*>(lw + L.l_qkv), d,
+                                         M, qd + 2 * kvd, d, eq, st);
+  ALR_LAUNCHED(ctx, "qkv gemm");
+
+  const AttnGeom g = geom(c);
+  {
+  ProfScope ps(ctx, decode ? ALR_PROF_DECODE_ATTN : ALR_PROF_PREFILL_ATTN, st);
+  if (!decode) {
+    if (mfma_attn(c)) {
+      const int nw = (int)ctx->h_pwork.size();
+      const PrefillItem* wk = ctx->at<PrefillItem>(L.i_pwork);
+      if constexpr (std::is_same<T, bf16>::value) {
+        if (hd == 128)
+          attn_prefill_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, at, wk, g);
+        else
+          attn_prefill_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, at, wk, g);
+      }
+    } else {
+      const long items = (long)M * H;
+      attn_generic_kernel<T><<<(unsigned)((items + 3) / 4), 256, 0, st>>>(
+          qb, kc, vc, nullptr, nullptr, 0, 0, ctx->at<int>(L.i_rowstart), nullptr, at, M, g);
+    }
+  } else {
+    if (mfma_attn(c)) {
+      const int nw = (int)ctx->h_dwork.size();
+      const DecodeItem* wk = ctx->at<DecodeItem>(L.i_dwork);
+      if constexpr (std::is_same<T, bf16>::value) {
+        if (hd == 128)
+          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, kp, vp, priv_rs, s,
+                                                            ctx->at<int>(L.i_apos), at, wk, g);
+        else
+          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, kp, vp, priv_rs, s,
+                                                           ctx->at<int>(L.i_apos), at, wk, g);
+      }
+    } else {
+      const long items = (long)M * H;
+      attn_generic_kernel<T><<<(unsigned)((items + 3) / 4), 256, 0, st>>>(
+          qb, kc, vc, kp, vp, priv_rs, s, ctx->at<int>(L.i_aseq), ctx->at<int>(L.i_apos), at, M,
+          g);
+    }
+  }
+  }
+  ALR_LAUNCHED(ctx, "attention");
+
+  EpiResid er;
+  er.h = resid;
+  er.ld = d;
+  er.feat = nullptr;
+  er.feat_rs = 0;
+  er.perm = nullptr;
+  if (decode)
+    launch_gemm<ALR_PROF_DECODE_O, T>(ctx, at, qd, reinterpret_cast<const T*>(lw + L.l_o), qd, M,
+                                      d, qd, er, st);
+  else
+    launch_gemm<ALR_PROF_PREFILL_O, T>(ctx, at, qd, reinterpret_cast<const T*>(lw + L.l_o), qd, M,
+                                       d, qd, er, st);
+  rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, reinterpret_cast<const T*>(lw + L.l_fnorm), xn, d,
+                                       c.rms_eps);
+  EpiSwiGLU<T> es;
+  es.out = act;
+  es.ld = F;
+  if (decode)
+    launch_gemm<ALR_PROF_DECODE_GU, T>(ctx, xn, d, reinterpret_cast<const T*>(lw + L.l_gu), d, M,
+                                       2 * F, d, es, st);
+  else
+    launch_gemm<ALR_PROF_PREFILL_GU, T>(ctx, xn, d, reinterpret_cast<const T*>(lw + L.l_gu), d, M,
+                                        2 * F, d, es, st);
+  er.feat = feat;
+  er.feat_rs = feat_rs;
+  er.perm = perm;
+  if (decode)
+    launch_gemm<ALR_PROF_DECODE_DOWN, T>(ctx, act, F, reinterpret_cast<const T*>(lw + L.l_down), F,
+                                         M, d, F, er, st);
+  else
+    launch_gemm<ALR_PROF_PREFILL_DOWN, T>(ctx, act, F, reinterpret_cast<const T*>(lw + L.l_down),
+                                          F, M, d, F, er, st);
+  ALR_LAUNCHED(ctx, "mlp");
+  return ALR_OK;
+}
+
+int feat_index(const alr_config& c, int l) {
+  for (int f = 0; f < c.n_feat; ++f)
+    if (c.feat_layers[f] == l) return f;
+  return -1;
+}
+
+template <typename T>
+alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* embeds,
+                        const uint8_t* mask, float* feats_out, hipStream_t st) {
+  const alr_config& c = ctx->cfg;
+  const Layout& L = ctx->L;
+  const int d = c.d_model, nf = c.n_feat;
+  embed_kernel<T><<<M, 256, 0, st>>>(ctx->at<float>(L.resid), tokens, ctx->at<T>(L.w_embed),
+                                     reinterpret_cast<const T*>(embeds), mask, d);
+  ALR_LAUNCHED(ctx, "embed");
+  for (int l = 0; l < c.n_layers; ++l) {
+    const int f = feat_index(c, l);
+    float* feat = f >= 0 ? ctx->at<float>(L.feat_store) + (long)f * d : nullptr;
+    const alr_status stt = layer_forward<T>(ctx, l, M, false, 0, feat, (long)nf * d, nullptr, st);
+    if (stt != ALR_OK) return stt;
+  }
+  rmsnorm_kernel<T><<<M, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
+                                       ctx->at<T>(L.hf_store), d, c.rms_eps);
+  ALR_LAUNCHED(ctx, "final norm");
+  if (feats_out && nf > 0)
+    ALR_HIP(ctx, hipMemcpyAsync(feats_out, ctx->at<float>(L.feat_store),
+                                (size_t)M * nf * d * sizeof(float), hipMemcpyDeviceToDevice, st));
+  return ALR_OK;
+}
+
+template <typename T>
+alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, int* tokens_out,
+                   float* logprobs_out, hipStream_t st) {
+  const alr_config& c = ctx->cfg;
+  const Layout& L = ctx->L;
+  const int V = c.vocab, d = c.d_model;
+  const int* perm = ctx->at<int>(L.i_perm);
+  EpiLogits el;
+  el.out = logprobs_out + (long)s * V;
+  el.rs = (long)block * V;
+  el.perm = perm;
+  launch_gemm<ALR_PROF_LM_GEMM, T>(ctx, ctx->at<T>(L.xnorm), d, ctx->at<T>(L.w_lm), d, n, V, d,
+                                   el, st);
+  {
+    ProfScope ps(ctx, ALR_PROF_LM_FINALIZE, st);
+    lm_finalize_kernel<<<n, 256, 0, st>>>(logprobs_out + (long)s * V, (long)block * V, perm, V,
+                                          tokens_out, block, s, forced, ctx->at<int>(L.i_cur));
+  }
+  ALR_LAUNCHED(ctx, "output head");
+  return ALR_OK;
+}
+
+template <typename T>
+alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, int32_t* tokens_out,
+                        float* logprobs_out, float* feats_out, hipStream_t st) {
+  const alr_config& c = ctx->cfg;
+  const Layout& L = ctx->L;
+  const int d = c.d_model, nf = c.n_feat;
+  const int* perm = ctx->at<int>(L.i_perm);
+  const int* atok = ctx->at<int>(L.i_atok);
+  // slot 0: the prefill's final-norm row and features at the anchor
+  gather_rows_kernel<T><<<n, 256, 0, st>>>(ctx->at<T>(L.xnorm), ctx->at<T>(L.hf_store), atok, d);
+  if (feats_out && nf > 0)
+    gather_feat_kernel<<<n, 256, 0, st>>>(feats_out, (long)block * nf * d, perm,
+                                          ctx->at<float>(L.feat_store), atok, (long)nf * d);
+  ALR_LAUNCHED(ctx, "slot-0 gather");
+  alr_status stt = lm_head<T>(ctx, n, 0, block, forced, tokens_out, logprobs_out, st);
+  if (stt != ALR_OK) return stt;
+  for (int s = 1; s < block; ++s) {
+    embed_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<int>(L.i_cur),
+                                       ctx->at<T>(L.w_embed), nullptr, nullptr, d);
+    ALR_LAUNCHED(ctx, "decode embed");
+    for (int l = 0; l < c.n_layers; ++l) {
+      const int f = feat_index(c, l);
+      float* feat = (f >= 0 && feats_out) ? feats_out + ((long)s * nf + f) * d : nullptr;
+      stt = layer_forward<T>(ctx, l, n, true, s, feat, (long)block * nf * d, perm, st);
+      if (stt != ALR_OK) return stt;
+    }
+    rmsnorm_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
+                                         ctx->at<T>(L.xnorm), d, c.rms_eps);
+    stt = lm_head<T>(ctx, n, s, block, forced, tokens_out, logprobs_out, st);
+    if (stt != ALR_OK) return stt;
+  }
+  return ALR_OK;
+}
+
+alr_status upload(alr_ctx* ctx, void* dst, const void* src, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return ALR_OK;
+  ALR_HIP(ctx, hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st));
+  return ALR_OK;
+}
+
+}  // namespace
+
+// ============================================================== C ABI
+
+extern "C" {
+
+const char* alr_status_string(alr_status st) {
+  switch (st) {
+    case ALR_OK: return "ALR_OK";
+    case ALR_E_INVALID_ARG: return "ALR_E_INVALID_ARG";
+    case ALR_E_OUT_OF_RANGE: return "ALR_E_OUT_OF_RANGE";
+    case ALR_E_WORKSPACE: return "ALR_E_WORKSPACE";
+    case ALR_E_STATE: return "ALR_E_STATE";
+    case ALR_E_UNSUPPORTED: return "ALR_E_UNSUPPORTED";
+    case ALR_E_HIP: return "ALR_E_HIP";
+  }
+  return "unknown status";
+}
+
+alr_status alr_check_config(const alr_config* cfg, char* msg, size_t msg_len) {
+  return check_config_impl(cfg, msg, msg_len);
+}
+
+size_t alr_workspace_bytes(const alr_config* cfg, const alr_limits* lim) {
+  if (check_config_impl(cfg, nullptr, 0) != ALR_OK || check_limits(lim, nullptr, 0) != ALR_OK)
+    return 0;
+  Layout L;
+  return compute_layout(*cfg, *lim, L);
+}
+
+alr_status alr_check_rollout(const alr_config* cfg, const alr_limits* lim, int32_t n_seq,
+                             const int32_t* seq_len, int32_t n_anchor, const int32_t* anchor_seq,
+                             const int32_t* anchor_pos, int32_t block, char* msg, size_t msg_len) {
+  alr_status st = check_config_impl(cfg, msg, msg_len);
+  if (st != ALR_OK) return st;
+  st = check_limits(lim, msg, msg_len);
+  if (st != ALR_OK) return st;
+  if (n_seq <= 0 || n_seq > lim->max_seqs)
+    return fmt_msg(msg, msg_len, "n_seq %d outside [1, %d]", n_seq, lim->max_seqs),
+           ALR_E_INVALID_ARG;
+  return check_rollout_impl(*cfg, *lim, n_seq, seq_len, n_anchor, anchor_seq, anchor_pos, block,
+                            msg, msg_len);
+}
+
+alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_limits* lim,
+                      void* workspace, size_t ws_bytes, alr_stream stream, alr_ctx** out) {
+  char msg[256];
+  if (!out) return fail(nullptr, ALR_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  alr_status st = check_config_impl(cfg, msg, sizeof(msg));
+  if (st != ALR_OK) return fail(nullptr, st, "%s", msg);
+  st = check_limits(lim, msg, sizeof(msg));
+  if (st != ALR_OK) return fail(nullptr, st, "%s", msg);
+  const alr_config& c = *cfg;
+  if (!w || !w->tok_embed || !w->final_norm || !w->lm_head)
+    return fail(nullptr, ALR_E_INVALID_ARG, "weights: tok_embed, final_norm and lm_head required");
+  if (c.n_layers > 0 && (!w->attn_norm || !w->wq || !w->wk || !w->wv || !w->wo || !w->ffn_norm ||
+                         !w->w_gate || !w->w_up || !w->w_down))
+    return fail(nullptr, ALR_E_INVALID_ARG, "weights: per-layer pointer arrays required");
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->ffn_norm[l] ||
+        !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
+      return fail(nullptr, ALR_E_INVALID_ARG, "weights of layer %d incomplete", l);
+  Layout L;
+  const size_t need = compute_layout(c, *lim, L);
+  if (!workspace) return fail(nullptr, ALR_E_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256)
+    return fail(nullptr, ALR_E_INVALID_ARG, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(nullptr, ALR_E_WORKSPACE, "workspace %zu bytes < required %zu", ws_bytes, need);
+
+  alr_ctx* ctx = new alr_ctx();
+  ctx->cfg = c;
+  ctx->lim = *lim;
+  ctx->ws = static_cast<char*>(workspace);
+  ctx->ws_bytes = ws_bytes;
+  ctx->L = L;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto bad = [&](alr_status e) {
+    g_create_err = ctx->err;
+    delete ctx;
+    return e;
+  };
+#define CREATE_HIP(call)                                                             \
+  do {                                                                               \
+    hipError_t e_ = (call);                                                          \
+    if (e_ != hipSuccess) {                                                          \
+      fail(ctx, ALR_E_HIP, "%s failed: %s", #call, hipGetErrorString(e_));           \
+      return bad(ALR_E_HIP);                                                         \
+    }                                                                                \
+  } while (0)
+
+  const size_t es = L.es, d = c.d_model, F = c.d_ffn, V = c.vocab;
+  const int H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
+  const size_t qd = (size_t)H * hd, kvd = (size_t)G * hd;
+  CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_embed, w->tok_embed, V * d * es, hipMemcpyDeviceToDevice, s));
+  CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_lm, w->lm_head, V * d * es, hipMemcpyDeviceToDevice, s));
+  CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_fnorm, w->final_norm, d * es, hipMemcpyDeviceToDevice, s));
+
+  // row maps (uploaded once, shared by all layers)
+  std::vector<int> qmap, kmap, maps;
+  rope_pair_rows(H, hd, qmap);
+  rope_pair_rows(G, hd, kmap);
+  maps.reserve(qd + 2 * kvd + 2 * F);
+  for (int x : qmap) maps.push_back(x);
+  for (int x : kmap) maps.push_back((int)qd + x);
+  for (size_t i = 0; i < kvd; ++i) maps.push_back((int)(qd + kvd + i));
+  for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + (i % 32)));       // gate
+  for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + 32 + (i % 32)));  // up
+  int* dmaps = ctx->at<int>(L.i_maps);
+  CREATE_HIP(hipMemcpyAsync(dmaps, maps.data(), maps.size() * 4, hipMemcpyHostToDevice, s));
+  const long rb = (long)d * es;
+  for (int l = 0; l < c.n_layers; ++l) {
+    char* lw = ctx->layer(l);
+    CREATE_HIP(hipMemcpyAsync(lw + L.l_anorm, w->attn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+    CREATE_HIP(hipMemcpyAsync(lw + L.l_fnorm, w->ffn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+    scatter_rows_kernel<<<(unsigned)qd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wq[l], dmaps, rb);
+    scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wk[l],
+                                                      dmaps + qd, rb);
+    scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wv[l],
+                                                      dmaps + qd + kvd, rb);
+    CREATE_HIP(hipMemcpyAsync(lw + L.l_o, w->wo[l], d * qd * es, hipMemcpyDeviceToDevice, s));
+    scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_gate[l],
+                                                    dmaps + qd + 2 * kvd, rb);
+    scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_up[l],
+                                                    dmaps + qd + 2 * kvd + F, rb);
+    CREATE_HIP(hipMemcpyAsync(lw + L.l_down, w->w_down[l], d * F * es, hipMemcpyDeviceToDevice, s));
+    CREATE_HIP(hipGetLastError());
+  }
+  // RoPE tables: angles in double, stored as float cos/sin [max_pos, hd/2]
+  {
+    const int half = hd / 2;
+    std::vector<float> cs((size_t)c.max_pos * half), sn((size_t)c.max_pos * half);
+    for (int i = 0; i < half; ++i) {
+      const double inv = std::pow((double)c.rope_base, -2.0 * i / hd);
+      for (int p = 0; p < c.max_pos; ++p) {
+        const double a = p * inv;
+        cs[(size_t)p * half + i] = (float)std::cos(a);
+        sn[(size_t)p * half + i] = (float)std::sin(a);
+      }
+    }
+    CREATE_HIP(hipMemcpyAsync(ctx->ws + L.rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, s));
+    CREATE_HIP(hipMemcpyAsync(ctx->ws + L.rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, s));
+    CREATE_HIP(hipStreamSynchronize(s));
+  }
+#undef CREATE_HIP
+  *out = ctx;
+  return ALR_OK;
+}
+
+alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, const int32_t* tokens,
+                       const void* embeds, const uint8_t* embed_mask, float* feats_out,
+                       alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  char msg[256];
+  alr_status st = check_prefill_impl(ctx->cfg, ctx->lim, n_seq, seq_len, tokens, embeds,
+                                     embed_mask, msg, sizeof(msg));
+  if (st != ALR_OK) return fail(ctx, st, "%s", msg);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const alr_config& c = ctx->cfg;
+  const int rep = c.n_heads / c.n_kv_heads;
+  ctx->prefilled = false;
+  ctx->n_seq = n_seq;
+  ctx->seq_len.assign(seq_len, seq_len + n_seq);
+  ctx->seq_off.assign(n_seq + 1, 0);
+  for (int i = 0; i < n_seq; ++i) ctx->seq_off[i + 1] = ctx->seq_off[i] + seq_len[i];
+  const int M = ctx->seq_off[n_seq];
+  ctx->h_tokpos.resize(M);
+  ctx->h_rowstart.resize(M);
+  ctx->h_pwork.clear();
+  for (int i = 0; i < n_seq; ++i) {
+    for (int p = 0; p < seq_len[i]; ++p) {
+      ctx->h_tokpos[ctx->seq_off[i] + p] = p;
+      ctx->h_rowstart[ctx->seq_off[i] + p] = ctx->seq_off[i];
+    }
+    const int n_items = ((seq_len[i] + 31) / 32) * rep;
+    for (int g = 0; g < c.n_kv_heads; ++g)
+      for (int it = 0; it < n_items; it += 4)
+        ctx->h_pwork.push_back(PrefillItem{ctx->seq_off[i], seq_len[i], g, it});
+  }
+  if (ctx->h_pwork.size() > ctx->L.max_pwork)
+    return fail(ctx, ALR_E_WORKSPACE, "prefill work list overflow");
+  const Layout& L = ctx->L;
+  st = upload(ctx, ctx->at<int>(L.i_tokpos), ctx->h_tokpos.data(), (size_t)M * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_rowstart), ctx->h_rowstart.data(), (size_t)M * 4, s);
+  if (st == ALR_OK)
+    st = upload(ctx, ctx->at<PrefillItem>(L.i_pwork), ctx->h_pwork.data(),
+                ctx->h_pwork.size() * sizeof(PrefillItem), s);
+  if (st != ALR_OK) return st;
+  st = (c.dtype == ALR_BF16) ? prefill_impl<bf16>(ctx, M, tokens, embeds, embed_mask, feats_out, s)
+                             : prefill_impl<float>(ctx, M, tokens, embeds, embed_mask, feats_out, s);
+  if (st == ALR_OK) ctx->prefilled = true;
+  return st;
+}
+
+alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                       const int32_t* anchor_pos, int32_t block, const int32_t* forced,
+                       int32_t* tokens_out, float* logprobs_out, float* feats_out,
+                       alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (!ctx->prefilled) return fail(ctx, ALR_E_STATE, "rollout before a successful prefill");
+  char msg[256];
+  alr_status st = check_rollout_impl(ctx->cfg, ctx->lim, ctx->n_seq, ctx->seq_len.data(), n_anchor,
+                                     anchor_seq, anchor_pos, block, msg, sizeof(msg));
+  if (st != ALR_OK) return fail(ctx, st, "%s", msg);
+  if (!tokens_out || !logprobs_out)
+    return fail(ctx, ALR_E_INVALID_ARG, "tokens_out and logprobs_out must not be NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const alr_config& c = ctx->cfg;
+  const int n = n_anchor;
+  std::vector<int> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  std::sort(order.begin(), order.end(), [&](int x, int y) {
+    if (anchor_seq[x] != anchor_seq[y]) return anchor_seq[x] < anchor_seq[y];
+    if (anchor_pos[x] != anchor_pos[y]) return anchor_pos[x] < anchor_pos[y];
+    return x < y;
+  });
+  ctx->h_anch.resize((size_t)4 * n);
+  int* perm = ctx->h_anch.data();
+  int* apos = perm + n;
+  int* atok = perm + 2 * n;
+  int* aseq = perm + 3 * n;
+  for (int r = 0; r < n; ++r) {
+    const int i = order[r];
+    perm[r] = i;
+    apos[r] = anchor_pos[i];
+    atok[r] = ctx->seq_off[anchor_seq[i]] + anchor_pos[i];
+    aseq[r] = ctx->seq_off[anchor_seq[i]];
+  }
+  ctx->h_dwork.clear();
+  const int ag = anchor_group(c);
+  for (int r0 = 0; r0 < n;) {
+    int r1 = r0;
+    while (r1 < n && anchor_seq[order[r1]] == anchor_seq[order[r0]]) ++r1;
+    for (int f = r0; f < r1; f += ag) {
+      const int cnt = std::min(ag, r1 - f);
+      for (int g = 0; g < c.n_kv_heads; ++g)
+        ctx->h_dwork.push_back(DecodeItem{f, cnt, g, aseq[f]});
+    }
+    r0 = r1;
+  }
+  if (ctx->h_dwork.size() > ctx->L.max_dwork)
+    return fail(ctx, ALR_E_WORKSPACE, "decode work list overflow");
+  const Layout& L = ctx->L;
+  // perm, apos, atok, aseq live in consecutive workspace arrays of max_anchors each
+  st = upload(ctx, ctx->at<int>(L.i_perm), perm, (size_t)n * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_apos), apos, (size_t)n * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_atok), atok, (size_t)n * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_aseq), aseq, (size_t)n * 4, s);
+  if (st == ALR_OK)
+    st = upload(ctx, ctx->at<DecodeItem>(L.i_dwork), ctx->h_dwork.data(),
+                ctx->h_dwork.size() * sizeof(DecodeItem), s);
+  if (st != ALR_OK) return st;
+  return (c.dtype == ALR_BF16)
+             ? rollout_impl<bf16>(ctx, n, block, forced, tokens_out, logprobs_out, feats_out, s)
+             : rollout_impl<float>(ctx, n, block, forced, tokens_out, logprobs_out, feats_out, s);
+}
+
+const char* alr_last_error(const alr_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_err.c_str();
+}
+
+void alr_destroy(alr_ctx* ctx) {
+  if (!ctx) return;
+  for (hipEvent_t e : ctx->prof_ev) (void)hipEventDestroy(e);
+  delete ctx;
+}
+
+// ------------------------------------------------------------------ debug hooks
+
+alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
+                          int32_t N, int32_t K, alr_stream stream) {
+  if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
+  if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  EpiLogits el;
+  el.out = C;
+  el.rs = N;
+  el.perm = nullptr;
+  alr_ctx dummy;
+  if (dtype == ALR_BF16)
+    launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, (const bf16*)W, K, M, N, K, el, s);
+  else if (dtype == ALR_F32)
+    launch_gemm<0, float>(&dummy, (const float*)A, K, (const float*)W, K, M, N, K, el, s);
+  else
+    return ALR_E_INVALID_ARG;
+  return hipGetLastError() == hipSuccess ? ALR_OK : ALR_E_HIP;
+}
+
+static void prof_release(alr_ctx* ctx) {
+  for (hipEvent_t e : ctx->prof_ev) (void)hipEventDestroy(e);
+  ctx->prof_ev.clear();
+  ctx->prof_used = 0;
+  ctx->prof_site = 0;
+}
+
+alr_status alr_profile_start(alr_ctx* ctx, int32_t site, int32_t capacity) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (site <= 0 || site >= ALR_PROF_COUNT || capacity <= 0)
+    return fail(ctx, ALR_E_INVALID_ARG, "profile site %d / capacity %d invalid", site, capacity);
+  prof_release(ctx);
+  ctx->prof_ev.resize((size_t)2 * capacity);
+  for (auto& e : ctx->prof_ev) {
+    const hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) {
+      e = nullptr;
+      prof_release(ctx);
+      return fail(ctx, ALR_E_HIP, "hipEventCreate failed: %s", hipGetErrorString(err));
+    }
+  }
+  ctx->prof_site = site;
+  return ALR_OK;
+}
+
+alr_status alr_profile_stop(alr_ctx* ctx, double* total_ms, int32_t* launches) {
+  if (!ctx || !total_ms || !launches) return ALR_E_INVALID_ARG;
+  double tot = 0.0;
+  const size_t n = ctx->prof_used;
+  if (n > 0) {
+    const hipError_t err = hipEventSynchronize(ctx->prof_ev[2 * n - 1]);
+    if (err != hipSuccess) {
+      prof_release(ctx);
+      return fail(ctx, ALR_E_HIP, "hipEventSynchronize failed: %s", hipGetErrorString(err));
+    }
+  }
+  for (size_t i = 0; i < n; ++i) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, ctx->prof_ev[2 * i], ctx->prof_ev[2 * i + 1]) == hipSuccess)
+      tot += ms;
+  }
+  *total_ms = tot;
+  *launches = (int32_t)n;
+  prof_release(ctx);
+  return ALR_OK;
+}
+
+}  // extern "C"

@@ -238,7 +238,7 @@ def _n_threads() -> int:
 
 
 def make_weights(shape: ModelShape, config_no: int, norm_gain: str = "ones",
-                 threads: Optional[int] = None) -> Dict:
+                 threads: Optional[int] = None, progress=None) -> Dict:
     """Draw all weights of ``shape`` from the workload's weight stream.
 
     Returns ``{"tok_embed", "lm_head", "final_norm", "layers": [dict per layer]}``;
@@ -254,7 +254,11 @@ def make_weights(shape: ModelShape, config_no: int, norm_gain: str = "ones",
         for (name, layer), ss in zip(names, children):
             jobs[(name, layer)] = ex.submit(_draw_matrix, ss, weight_shape(shape, name),
                                             0.02, shape.dtype)
-        res = {k: v.result() for k, v in jobs.items()}
+        res = {}
+        for i, (k, v) in enumerate(jobs.items()):
+            res[k] = v.result()
+            if progress is not None and (i + 1) % 32 == 0:
+                progress(f"weights: {i + 1}/{len(jobs)} tensors drawn")
 
     def gain(i: int) -> np.ndarray:
         if norm_gain == "ones":
@@ -336,11 +340,11 @@ class Inputs:
     embed_mask: Optional[np.ndarray]  # uint8 [n_seq*seq_len] or None
 
 
-def make_inputs(w, norm_gain: str = "ones") -> Inputs:
+def make_inputs(w, norm_gain: str = "ones", progress=None) -> Inputs:
     if not isinstance(w, Workload):
         w = get(w)
     wcfg = w.weight_seed_config or w.config_no
-    weights = make_weights(w.shape, wcfg, norm_gain=norm_gain)
+    weights = make_weights(w.shape, wcfg, norm_gain=norm_gain, progress=progress)
     a_seq, a_pos = make_anchors(w)
     emb, mask = make_image_rows(w)
     return Inputs(w, weights, make_tokens(w), a_seq, a_pos, emb, mask)

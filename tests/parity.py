@@ -1,0 +1,121 @@
+"""Helpers that run the HIP path and the CPU oracle on the same seeded inputs and compare them.
+
+Parity rules (fp32 / bf16):
+
+* tokens: bit-exact wherever the oracle's top-1 margin (in log-prob) exceeds
+  ``tok_margin`` (1e-4 fp32, 1e-2 bf16, raised to 2x the measured bf16 noise
+  floor when that is larger).  Where the margin is smaller the GPU's token
+  must be an epsilon-argmax of the oracle's distribution; the comparison then
+  continues with the GPU re-run on the oracle's tokens (``forced``), so that
+  both sides condition on the same path.
+* log-probs: max-abs difference <= ``lp_tol`` (1e-4 fp32; bf16: max(2e-2,
+  2x floor)).
+* features: max-abs difference, divided by the RMS of the oracle's feature row
+  for bf16, <= ``ft_tol``.
+
+The bf16 noise floor is the difference between two valid bf16 evaluations of
+the same model that round at the same points but accumulate in different
+precisions (oracle with fp64 vs fp32 working precision).
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+import oracle as O
+
+
+@dataclasses.dataclass
+class Report:
+    n_slots: int
+    lp_max_abs: float
+    ft_max: float
+    tok_mismatch_confident: int
+    tok_near_tie: int
+    floor_lp: float
+    floor_ft: float
+    lp_tol: float
+    ft_tol: float
+    tok_margin: float
+    forced_rerun: bool
+
+    def ok(self) -> bool:
+        return (self.lp_max_abs <= self.lp_tol and self.ft_max <= self.ft_tol
+                and self.tok_mismatch_confident == 0)
+
+
+def _given(inp, sel_seq):
+    if inp.embeds is None:
+        return None, None
+    w = inp.workload
+    rows = inp.embeds.reshape(w.n_seq, w.seq_len, -1)
+    mask = inp.embed_mask.reshape(w.n_seq, w.seq_len)
+    return rows, mask
+
+
+def oracle_rollout(inp, shape, anchor_seq, anchor_pos, block, feed, emulate, dt=np.float64):
+    """Teacher-forced oracle along ``feed`` (tokens fed after each slot)."""
+    P = O.Params(inp.weights, dt=dt, cache=shape.n_params() < 400_000_000)
+    rows, mask = _given(inp, anchor_seq)
+    return O.rollout_teacher_forced(P, shape, inp.tokens, anchor_seq, anchor_pos, block, feed,
+                                    given_rows=rows, given_mask=mask, emulate_bf16=emulate)
+
+
+def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = None) -> Report:
+    """Compare the GPU rollout of anchors ``sel`` (indices into the workload's anchors).
+
+    gpu_run(forced or None) -> (tokens [n,B], logprobs [n,B,V], feats [n,B,nf,d]) as numpy,
+    for exactly the selected anchors.
+    """
+    bf16 = shape.dtype == "bf16"
+    a_seq = inp.anchor_seq[sel]
+    a_pos = inp.anchor_pos[sel]
+    g_tok, g_lp, g_ft = gpu_run(None)
+    # oracle along the GPU's own path: equals the naive definition wherever they agree
+    o_tok, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, bf16)
+    floor_lp = floor_ft = 0.0
+    if bf16 and (measure_floor is None or measure_floor):
+        e_tok, e_lp, e_ft, _ = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, True,
+                                              dt=np.float32)
+        floor_lp = float(np.abs(e_lp - o_lp).max())
+        rms = np.sqrt(np.mean(o_ft ** 2, axis=-1, keepdims=True)) if o_ft.size else 1.0
+        floor_ft = float((np.abs(e_ft - o_ft) / rms).max()) if o_ft.size else 0.0
+    if bf16:
+        tok_margin = max(1e-2, 2 * floor_lp)
+        lp_tol = max(2e-2, 2 * floor_lp)
+        ft_tol = max(2e-2, 2 * floor_ft)
+    else:
+        tok_margin, lp_tol, ft_tol = 1e-4, 1e-4, 1e-4
+    # which slots are confident, which are near-ties
+    conf = margin > tok_margin
+    mism = g_tok != o_tok
+    confident_bad = int((mism & conf).sum())
+    near = mism & ~conf
+    # near-ties must be epsilon-argmaxes
+    if near.any():
+        idx = np.nonzero(near)
+        top = o_lp[idx].max(axis=-1)
+        chosen = o_lp[idx[0], idx[1], g_tok[idx]]
+        confident_bad += int((chosen < top - tok_margin).sum())
+    forced_rerun = False
+    if near.any():
+        # continue on the oracle's path: feed the oracle's own tokens to both sides
+        forced = o_tok.astype(np.int32).copy()
+        g_tok, g_lp, g_ft = gpu_run(forced)
+        o_tok2, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, forced, bf16)
+        conf = margin > tok_margin
+        confident_bad += int(((g_tok != o_tok2) & conf).sum())
+        forced_rerun = True
+    lp_err = float(np.abs(g_lp - o_lp).max())
+    if o_ft.size:
+        if bf16:
+            rms = np.sqrt(np.mean(o_ft ** 2, axis=-1, keepdims=True))
+            ft_err = float((np.abs(g_ft - o_ft) / rms).max())
+        else:
+            ft_err = float(np.abs(g_ft - o_ft).max())
+    else:
+        ft_err = 0.0
+    return Report(int(np.prod(g_tok.shape)), lp_err, ft_err, confident_bad, int(near.sum()),
+                  floor_lp, floor_ft, lp_tol, ft_tol, tok_margin, forced_rerun)
