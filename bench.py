@@ -52,24 +52,55 @@ def site_work(site: str, w) -> dict:
     raise KeyError(site)
 
 
-def cpu_baseline(inp, budget_layers=(1, 2)):
-    """Time the oracle (teacher-forced, fp64) on one anchor with the model truncated to
-    1 and 2 decoder layers; extrapolate linearly in depth to the full model."""
+# rocprofv3 counter summaries: launch site -> (summary file, kernel sources it was taken on)
+PROFILE_FILES = {
+    "prefill_gu": ("profiles/gemm_gate_up_prefill_llama8b_like.md",
+                   ("paper_2609_38795_amd/csrc/gemm_kernels.hpp",
+                    "paper_2609_38795_amd/csrc/device_common.hpp")),
+}
+
+
+def measured_traffic(site: str):
+    """HBM bytes per launch from the committed counter summary, or None when the kernel
+    source has changed since the counters were taken (or none were taken)."""
+    import hashlib
+    import re
+
+    if site not in PROFILE_FILES:
+        return None
+    path, srcs = PROFILE_FILES[site]
+    try:
+        text = open(os.path.join(ROOT, path)).read()
+        h = hashlib.sha256()
+        for f in srcs:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+    except OSError:
+        return None
+    m_t = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    m_h = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    if not m_t or not m_h or m_h.group(1) != h.hexdigest()[:16]:
+        return None
+    return float(m_t.group(1))
+
+
+def cpu_baseline(inp, budget_layers=(2, 8), n_anchors=2):
+    """Time the oracle (teacher-forced, fp64) on the anchors with the shortest prefixes,
+    with the model cut to two depths; extrapolate linearly in depth to the full model."""
     import numpy as np
 
     import oracle as O
     from paper_2609_38795_amd import workloads as W
 
     w = inp.workload
-    i = int(np.argmin(inp.anchor_pos))  # the anchor with the shortest prefix
-    a_seq, a_pos = inp.anchor_seq[i:i + 1], inp.anchor_pos[i:i + 1]
-    feed = np.zeros((1, w.block), np.int64)
+    sel = np.argsort(inp.anchor_pos, kind="stable")[:n_anchors]  # shortest prefixes
+    a_seq, a_pos = inp.anchor_seq[sel], inp.anchor_pos[sel]
+    feed = np.zeros((len(sel), w.block), np.int64)
     rows = mask = None
     if inp.embeds is not None:
         rows = inp.embeds.reshape(w.n_seq, w.seq_len, -1)
         mask = inp.embed_mask.reshape(w.n_seq, w.seq_len)
     times = {}
-    for nl in budget_layers:
+    for nl in sorted({min(x, w.shape.n_layers) for x in budget_layers}):
         shape = W.scaled(w, "trunc", n_layers=nl, feat_layers=tuple(range(min(nl, 1)))).shape
         wt = dict(inp.weights)
         wt["layers"] = inp.weights["layers"][:nl]
@@ -80,20 +111,30 @@ def cpu_baseline(inp, budget_layers=(1, 2)):
                                  emulate_bf16=(w.shape.dtype == "bf16"))
         times[nl] = time.perf_counter() - t0
     l1, l2 = budget_layers
+    l1, l2 = min(l1, w.shape.n_layers), min(l2, w.shape.n_layers)
+    if l1 == l2:
+        t_full = times[l1]
+        return _cpu_result(w, t_full, len(sel), a_pos, times, l1, l2)
     per_layer = (times[l2] - times[l1]) / (l2 - l1)
     fixed = times[l1] - l1 * per_layer
     t_full = fixed + w.shape.n_layers * per_layer
+    return _cpu_result(w, t_full, len(sel), a_pos, times, l1, l2)
+
+
+def _cpu_result(w, t_full, n, a_pos, times, l1, l2):
     try:
         from threadpoolctl import threadpool_info
 
         cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) or 1
     except Exception:
         cores = os.cpu_count() or 1
-    return {"value": w.block / t_full, "unit": "rollout slots/s", "cores": cores, "kind": "oracle",
-            "sample": (f"fp64 teacher-forced oracle, 1 anchor (position {int(a_pos[0])}, "
-                       f"{w.block} slots) with the model cut to {l1} and {l2} decoder layers "
-                       f"({times[l1]:.1f} s, {times[l2]:.1f} s), extrapolated linearly to "
-                       f"{w.shape.n_layers} layers ({t_full:.1f} s per anchor)")}
+    return {"value": n * w.block / t_full, "unit": "rollout slots/s", "cores": cores,
+            "kind": "oracle",
+            "sample": (f"fp64 bf16-emulating teacher-forced oracle on the {n} anchors with the "
+                       f"shortest prefixes (positions {', '.join(str(int(p)) for p in a_pos)}; "
+                       f"{w.block} slots each) with the model cut to {l1} and {l2} decoder "
+                       f"layers ({times[l1]:.1f} s, {times[l2]:.1f} s), extrapolated linearly "
+                       f"to {w.shape.n_layers} layers ({t_full:.1f} s)")}
 
 
 def main():
@@ -105,6 +146,8 @@ def main():
     ap.add_argument("--site", default="prefill_gu", help="kernel launch site for the roofline")
     ap.add_argument("--breakdown", action="store_true", help="time every launch site (extra steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
@@ -191,9 +234,20 @@ def main():
         achieved = work["bytes"] / avg_s / 1e9
         peak = PEAK_HBM_GBS
     roofline = {"bound": work["bound"], "achieved": round(achieved, 2), "peak": peak,
-                "unit": work["unit"], "frac": round(achieved / peak, 4), "traffic": None,
+                "unit": work["unit"], "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic(args.site),
                 "kernel": args.site, "avg_launch_ms": round(avg_s * 1e3, 4),
                 "launches_timed": site_n}
+
+    if args.copy_calibration:
+        n = 1 << 28  # 2^28 fp32 = 1 GiB read + 1 GiB written per launch
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log(f"[bench] copy calibration: 3 launches of {4 * n} bytes read + written")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:
