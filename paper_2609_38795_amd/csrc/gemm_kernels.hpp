@@ -1,8 +1,8 @@
 // GEMM kernels C[M,N] = A[M,K] * W[N,K]^T with fused epilogues (gfx950).
 //
-// bf16 path: 32x32x16 bf16 MFMA, 128x128x64 workgroup tile, 4 waves as 2x2,
-// each wave a 64x64 sub-tile (2x2 MFMA blocks).  fp32 path: FMA, 64x64x16
-// tile.  Both hand the epilogue *pairs* of outputs: the value at column c and
+// bf16 path: 32x32x16 bf16 MFMA, workgroup tiles from 64x128 to 256x128 chosen
+// per shape, 4 waves, each wave a (BM/WGM) x 64 sub-tile.  fp32 path: FMA,
+// 64x64x16 tile.  Both hand the epilogue *pairs* of outputs: the value at column c and
 // the one at column c+32, where c lies in the low half of a 64-column group.
 // Weight rows are arranged at context creation so that every fused operation
 // needs exactly such a pair: SwiGLU's gate/up values and RoPE's rotate-half
@@ -108,9 +108,18 @@ struct EpiLogits {
 };
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
-
-constexpr int GB_M = 128, GB_N = 128, GB_K = 64;
-constexpr int GB_PITCH = GB_K + 8;  // bf16 elements per LDS row (144 bytes)
+//
+// Workgroup tile BM x BN, WGM x WGN waves, wave tile (BM/WGM) x (BN/WGN) with a
+// width that is a multiple of 64 so the epilogue pairs c and c+32 sit in one
+// lane.
+// K is consumed in steps of BK through two LDS stages.  Global loads run two
+// steps ahead into two register sets; the steady-state loop handles two steps
+// per iteration with no data-dependent branches (prefetch offsets are clamped
+// to the last step, so the final iterations re-read it harmlessly), which
+// keeps the compiler's wait counting exact.  Within a step the LDS fragments
+// of k-slice ks+1 are read while the MFMAs of slice ks run.  LDS rows of BK
+// bf16 are XOR-swizzled in 16-byte chunks so ds_read_b128 / ds_write_b128 are
+// free of bank conflicts.
 
 // Tile order: workgroups are dispatched round-robin over the 8 XCDs, so the
 // block id is first remapped to make each XCD walk a contiguous range of the
@@ -130,100 +139,186 @@ __device__ __forceinline__ void gemm_tile_coords(int tiles_m, int tiles_n, int& 
   tn = in / gm;
 }
 
+// Element offset of 16-byte chunk c of LDS row r for rows of BK bf16.
+//  BK = 32 (4 chunks, 64 B): h = ((r>>2)&1)<<1 | ((r>>1)^(r>>3))&1
+//  BK = 64 (8 chunks, 128 B): h = (r & 7) ^ ((r >> 3) & 1)
+// Either way the 16 rows a 16-lane group reads with one ds_read_b128 cover all
+// 16 granules of a 256-byte LDS line, and 8 aligned rows cover the 8
+// granules of a 128-byte line.
+template <int BK>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (BK == 32) {
+    const int h = (((r >> 2) & 1) << 1) | (((r >> 1) ^ (r >> 3)) & 1);
+    return r * 32 + ((c ^ h) << 3);
+  } else {
+    const int h = (r & 7) ^ ((r >> 3) & 1);
+    return r * 64 + ((c ^ h) << 3);
+  }
+}
+
+template <int CH>
+struct GemmRegs {
+  u32x4 v[CH];
+};
+
+template <int CH>
+__device__ __forceinline__ void gemm_gload(GemmRegs<CH>& r, const bf16* const* src, int ko) {
+#pragma unroll
+  for (int i = 0; i < CH; ++i) r.v[i] = *(const u32x4*)(src[i] + ko);
+}
+
+template <int CH>
+__device__ __forceinline__ void gemm_lstore(const GemmRegs<CH>& r, bf16* stage, const int* off) {
+#pragma unroll
+  for (int i = 0; i < CH; ++i) *(u32x4*)(stage + off[i]) = r.v[i];
+}
+
+template <int MI, int NI>
+struct GemmFrag {
+  bf16x8 a[MI], b[NI];
+};
+
+template <int BK, int MI, int NI, int WTM, int WTN>
+__device__ __forceinline__ void gemm_frag_load(GemmFrag<MI, NI>& f, const bf16* As,
+                                               const bf16* Ws, int wm, int wn, int ks) {
+  const int lane = threadIdx.x & 63, lr = lane & 31, lh = lane >> 5;
+  const int c = ks * 2 + lh;
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+    f.a[mi] = as_bf16x8(*(const u32x4*)(As + swz<BK>(wm * WTM + mi * 32 + lr, c)));
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni)
+    f.b[ni] = as_bf16x8(*(const u32x4*)(Ws + swz<BK>(wn * WTN + ni * 32 + lr, c)));
+}
+
+template <int MI, int NI>
+__device__ __forceinline__ void gemm_frag_mma(const GemmFrag<MI, NI>& f,
+                                              f32x16 (&acc)[MI][NI]) {
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma32x32x16(f.a[mi], f.b[ni], acc[mi][ni]);
+}
+
+// MFMAs of one LDS stage, k-slice by k-slice, reading the fragments of slice
+// ks+1 while slice ks runs, and writing the next step's operand registers
+// (ra, rw) into the other LDS stage a few chunks per slice so the LDS writes
+// overlap the MFMAs instead of bunching up before the barrier.
+template <int BK, int MI, int NI, int WTM, int WTN, int A_CH, int W_CH>
+__device__ __forceinline__ void gemm_stage_mma(const bf16* As, const bf16* Ws, int wm, int wn,
+                                               f32x16 (&acc)[MI][NI], const GemmRegs<A_CH>& ra,
+                                               const GemmRegs<W_CH>& rw, bf16* As_nx, bf16* Ws_nx,
+                                               const int* a_off, const int* w_off) {
+  constexpr int KS = BK / 16;
+  GemmFrag<MI, NI> f[2];
+  gemm_frag_load<BK, MI, NI, WTM, WTN>(f[0], As, Ws, wm, wn, 0);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + 1 < KS) gemm_frag_load<BK, MI, NI, WTM, WTN>(f[(ks + 1) & 1], As, Ws, wm, wn, ks + 1);
+    gemm_frag_mma<MI, NI>(f[ks & 1], acc);
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i)
+      if (i % KS == ks) *(u32x4*)(As_nx + a_off[i]) = ra.v[i];
+#pragma unroll
+    for (int i = 0; i < W_CH; ++i)
+      if (i % KS == ks) *(u32x4*)(Ws_nx + w_off[i]) = rw.v[i];
+    __builtin_amdgcn_sched_barrier(0);  // keep each slice's writes with its MFMAs
+  }
+}
+
 // TAG only separates the instantiations of different call sites, so that
-// profilers report each GEMM of the model on its own line.
-template <int TAG, class Epi>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(const bf16* __restrict__ A, int lda,
-                                                        const bf16* __restrict__ W, int ldw,
-                                                        int M, int N, int K, int tiles_m,
-                                                        int tiles_n, Epi epi) {
-  __shared__ __attribute__((aligned(16))) bf16 As[GB_M * GB_PITCH];
-  __shared__ __attribute__((aligned(16))) bf16 Ws[GB_N * GB_PITCH];
+// profilers report each GEMM of the model on its own line.  K must be a
+// multiple of 2*BK.
+template <int TAG, int BM, int BN, int WGM, int WGN, int BK, int OCC, class Epi>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
+    int tiles_m, int tiles_n, Epi epi) {
+  constexpr int NT = 64 * WGM * WGN;  // threads
+  constexpr int WTM = BM / WGM;  // wave tile rows
+  constexpr int WTN = BN / WGN;  // wave tile columns (multiple of 64: epilogue pairs c, c+32)
+  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
+  constexpr int MI = WTM / 32;   // 32x32 blocks per wave along M
+  constexpr int NI = WTN / 32;   // and along N
+  constexpr int CPR = BK / 8;    // 16-byte chunks per row
+  constexpr int A_CH = BM * CPR / NT, W_CH = BN * CPR / NT;  // chunks per thread
+  static_assert(A_CH >= 1 && W_CH >= 1 && A_CH * NT == BM * CPR && W_CH * NT == BN * CPR,
+                "tile does not split evenly over the threads");
+  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) bf16 Ws[2][BN * BK];
+
   int tm, tn;
   gemm_tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * GB_M, n0 = tn * GB_N;
+  const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
-  // global -> register staging: 4 chunks of 16 bytes per operand per thread
-  u32x4 ra[4], rw[4];
-  const bf16* a_src[4];
-  const bf16* w_src[4];
-  int lds_off[4];
+  const bf16* a_src[A_CH];
+  const bf16* w_src[W_CH];
+  int a_off[A_CH], w_off[W_CH];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ch = tid + 256 * i;
-    const int r = ch >> 3, c8 = (ch & 7) * 8;
-    const int ar = min(m0 + r, M - 1), wr = min(n0 + r, N - 1);
-    a_src[i] = A + (long)ar * lda + c8;
-    w_src[i] = W + (long)wr * ldw + c8;
-    lds_off[i] = r * GB_PITCH + c8;
-  }
-  const int nk = K / GB_K;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = *(const u32x4*)(a_src[i]);
-    rw[i] = *(const u32x4*)(w_src[i]);
+  for (int i = 0; i < A_CH; ++i) {
+    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
+    a_src[i] = A + (long)min(m0 + r, M - 1) * lda + c * 8;
+    a_off[i] = swz<BK>(r, c);
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    *(u32x4*)(As + lds_off[i]) = ra[i];
-    *(u32x4*)(Ws + lds_off[i]) = rw[i];
+  for (int i = 0; i < W_CH; ++i) {
+    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
+    w_src[i] = W + (long)min(n0 + r, N - 1) * ldw + c * 8;
+    w_off[i] = swz<BK>(r, c);
   }
+  const int nk = K / BK;  // even, >= 2
+  const int klast = (nk - 1) * BK;
+
+  GemmRegs<A_CH> ra0, ra1;
+  GemmRegs<W_CH> rw0, rw1;
+  gemm_gload(ra0, a_src, 0);
+  gemm_gload(rw0, w_src, 0);
+  gemm_gload(ra1, a_src, BK);
+  gemm_gload(rw1, w_src, BK);
+  gemm_lstore(ra0, As[0], a_off);
+  gemm_lstore(rw0, Ws[0], w_off);
   __syncthreads();
 
-  f32x16 acc[2][2];
+  f32x16 acc[MI][NI];
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int ni = 0; ni < NI; ++ni)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
 
-  const int lr = lane & 31, lk = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) {
-      const int ko = (kt + 1) * GB_K;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra[i] = *(const u32x4*)(a_src[i] + ko);
-        rw[i] = *(const u32x4*)(w_src[i] + ko);
-      }
-    }
-#pragma unroll
-    for (int ks = 0; ks < GB_K / 16; ++ks) {
-      bf16x8 av[2], bv[2];
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-        av[mi] = as_bf16x8(*(const u32x4*)(As + (wm * 64 + mi * 32 + lr) * GB_PITCH + ks * 16 + lk));
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-        bv[ni] = as_bf16x8(*(const u32x4*)(Ws + (wn * 64 + ni * 32 + lr) * GB_PITCH + ks * 16 + lk));
-#pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni) acc[mi][ni] = mfma32x32x16(av[mi], bv[ni], acc[mi][ni]);
-    }
+  for (int kt = 0; kt < nk; kt += 2) {
+    // step kt from stage 0; set 0 refills with step kt+2; set 1 (step kt+1) -> stage 1
+    const int k2 = min((kt + 2) * BK, klast), k3 = min((kt + 3) * BK, klast);
+    gemm_gload(ra0, a_src, k2);
+    gemm_gload(rw0, w_src, k2);
+    __builtin_amdgcn_sched_barrier(0);  // keep the prefetch at the top of the step
+    gemm_stage_mma<BK, MI, NI, WTM, WTN, A_CH, W_CH>(As[0], Ws[0], wm, wn, acc, ra1, rw1, As[1],
+                                                     Ws[1], a_off, w_off);
     __syncthreads();
-    if (kt + 1 < nk) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *(u32x4*)(As + lds_off[i]) = ra[i];
-        *(u32x4*)(Ws + lds_off[i]) = rw[i];
-      }
-    }
+    // step kt+1 from stage 1; set 1 refills with step kt+3; set 0 (step kt+2) -> stage 0
+    gemm_gload(ra1, a_src, k3);
+    gemm_gload(rw1, w_src, k3);
+    __builtin_amdgcn_sched_barrier(0);
+    gemm_stage_mma<BK, MI, NI, WTM, WTN, A_CH, W_CH>(As[1], Ws[1], wm, wn, acc, ra0, rw0, As[0],
+                                                     Ws[0], a_off, w_off);
     __syncthreads();
   }
 
-  const int col = n0 + wn * 64 + lr;
-  if (col < N) {
+  const int lr = lane & 31, lh = lane >> 5;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+  for (int nj = 0; nj < NI / 2; ++nj) {
+    const int col = n0 + wn * WTN + nj * 64 + lr;
+    if (col < N) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M) epi(row, col, acc[mi][0][r], acc[mi][1][r]);
-      }
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
+        }
+    }
   }
 }
 

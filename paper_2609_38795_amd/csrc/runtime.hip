@@ -294,12 +294,36 @@ struct ProfScope {
 
 template <int TAG, typename T, class Epi>
 void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, int N, int K,
-                 Epi epi, hipStream_t st) {
+                 Epi epi, hipStream_t st, int force_tile = 0) {
   if (M <= 0) return;
   ProfScope ps(ctx, TAG, st);
   if constexpr (std::is_same<T, bf16>::value) {
-    const int tm = (M + GB_M - 1) / GB_M, tn = (N + GB_N - 1) / GB_N;
-    gemm_bf16_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+    // largest tile that still fills the 256 CUs: 256x256 (8 waves) for the
+    // prefill and the wide decode GEMMs, 128x128 otherwise; BK = 64 where K
+    // allows an even number of 64-deep steps
+    auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
+    int cfg = force_tile;
+    if (cfg == 0) cfg = tiles(256, 256) >= 256 ? 4 : (tiles(128, 128) >= 256 ? 2 : 3);
+    const bool k64 = (K % 128) == 0;
+    const int bm = (cfg == 1 || cfg >= 4) ? 256 : (cfg == 2 ? 128 : 64);
+    const int bn = cfg >= 4 ? 256 : 128;
+    const int tm = (M + bm - 1) / bm, tn = (N + bn - 1) / bn;
+    const int nb = tm * tn;
+#define ALR_GEMM(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                      \
+  gemm_bf16_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                          \
+      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
+    if (cfg == 5) {
+      if (k64) ALR_GEMM(256, 256, 2, 2, 64, 1); else ALR_GEMM(256, 256, 2, 2, 32, 1);
+    } else if (cfg == 4) {
+      if (k64) ALR_GEMM(256, 256, 2, 4, 64, 1); else ALR_GEMM(256, 256, 2, 4, 32, 1);
+    } else if (cfg == 1) {
+      if (k64) ALR_GEMM(256, 128, 2, 2, 64, 1); else ALR_GEMM(256, 128, 2, 2, 32, 1);
+    } else if (cfg == 2) {
+      if (k64) ALR_GEMM(128, 128, 2, 2, 64, 2); else ALR_GEMM(128, 128, 2, 2, 32, 2);
+    } else {
+      if (k64) ALR_GEMM(64, 128, 2, 2, 64, 2); else ALR_GEMM(64, 128, 2, 2, 32, 4);
+    }
+#undef ALR_GEMM
   } else {
     const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
     gemm_f32_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
@@ -822,7 +846,7 @@ void alr_destroy(alr_ctx* ctx) {
 // ------------------------------------------------------------------ debug hooks
 
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
-                          int32_t N, int32_t K, alr_stream stream) {
+                          int32_t N, int32_t K, int32_t tile, alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -832,7 +856,8 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   el.perm = nullptr;
   alr_ctx dummy;
   if (dtype == ALR_BF16)
-    launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, (const bf16*)W, K, M, N, K, el, s);
+    launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, (const bf16*)W, K, M, N, K, el, s,
+                         tile >= 0 && tile <= 5 ? tile : 0);
   else if (dtype == ALR_F32)
     launch_gemm<0, float>(&dummy, (const float*)A, K, (const float*)W, K, M, N, K, el, s);
   else
