@@ -106,61 +106,118 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 // lane-local reduction plus one exchange with lane ^ 32.  O^T = V^T P^T then
 // keeps the same column-per-query layout, so rescaling by the running max is
 // lane-local too.  P^T is fed to the second MFMA straight from the first
-// one's accumulators: in k-step ks (16 keys) lane half h supplies keys
-// {4h..4h+3, 8+4h..8+4h+3} (+16 ks), and V^T is read from LDS in the same key
-// order, which leaves the sum unchanged.
+// one's accumulators: in a 16-key k-step lane half h supplies keys
+// {4h..4h+3, 8+4h..8+4h+3}; the V^T tile keeps its keys in that order inside
+// each 16-key group, so each V^T operand is one 16-byte LDS read.
 //
-// A workgroup has 4 waves; wave w owns 32 query rows.  Key tiles of 64 keys
-// are staged in LDS: K as [key][hd] rows, V transposed as [hd][key].
+// The shared V cache is stored transposed, [G][hd][column] per layer, with
+// every sequence's columns starting at a multiple of 64, so a 64-key V^T tile
+// is 16-byte loads of contiguous keys.  K tiles are [key][hd].  Both tiles are
+// XOR-swizzled in 16-byte chunks so the MFMA operand reads are free of LDS
+// bank conflicts.  Tiles are double-buffered: the next tile's global loads are
+// in flight while the current one is consumed.
 
 constexpr int AT_KT = 64;
+constexpr int AT_DECODE_CHUNK = 512;  // keys per decode work item
+
+template <int NCH>
+__device__ __forceinline__ int chunk_swz(int r, int c) {
+  if constexpr (NCH == 16)
+    return c ^ (r & 15);
+  else
+    return c ^ ((r & 7) ^ ((r >> 3) & 1));
+}
 
 template <int HD>
-struct AttnSmem {
-  static constexpr int KP = HD + 8;      // K row pitch (bf16)
-  static constexpr int VP = AT_KT + 8;   // V^T row pitch (bf16)
-  bf16 k[AT_KT * KP];
-  bf16 vt[HD * VP];
+struct AttnTile {
+  bf16 k[AT_KT * HD];   // [key][dim]
+  bf16 vt[HD * AT_KT];  // [dim][key]
 };
 
-// Cooperative load of one K/V tile (keys key0 .. key0+63 of rows base_row+key,
-// clamped to max_row) into LDS.
 template <int HD>
-__device__ __forceinline__ void attn_load_tile(AttnSmem<HD>& sm, const bf16* __restrict__ Kc,
-                                               const bf16* __restrict__ Vc, long kv_rs, int kvh,
-                                               long base_row, int key0, int max_key) {
-  constexpr int CH = AT_KT * HD / 8;  // 16-byte chunks
-  for (int ch = threadIdx.x; ch < CH; ch += 256) {
-    const int key = ch / (HD / 8), d8 = (ch % (HD / 8)) * 8;
-    const long r = base_row + min(key0 + key, max_key);
-    const u32x4 kv = *(const u32x4*)(Kc + r * kv_rs + (long)kvh * HD + d8);
-    *(u32x4*)(sm.k + key * AttnSmem<HD>::KP + d8) = kv;
-    const u32x4 vv = *(const u32x4*)(Vc + r * kv_rs + (long)kvh * HD + d8);
+struct AttnStage {
+  u32x4 k[HD / 32];
+  u32x4 v[HD / 32];
+};
+
+// Global loads of one tile: keys k0..k0+63 of a sequence whose key 0 is token
+// row krow0 of the K cache and column vcol0 of the V^T cache.  Keys beyond
+// max_key read a clamped K row and zeros for V (they are masked anyway; the
+// zeros keep unwritten padding out of the sums).
+template <int HD>
+__device__ __forceinline__ void attn_gload(AttnStage<HD>& st, const bf16* __restrict__ Kc,
+                                           long kv_rs, int kvh, long krow0,
+                                           const bf16* __restrict__ vT, long vt_stride,
+                                           long vcol0, int k0, int max_key) {
+  constexpr int NCHK = HD / 8;
+  const int tid = threadIdx.x;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      sm.vt[(d8 + 2 * e) * AttnSmem<HD>::VP + key] = (bf16)(vv[e] & 0xFFFFu);
-      sm.vt[(d8 + 2 * e + 1) * AttnSmem<HD>::VP + key] = (bf16)(vv[e] >> 16);
+  for (int i = 0; i < HD / 32; ++i) {
+    const int ch = tid + 256 * i, key = ch / NCHK, c = ch % NCHK;
+    st.k[i] = *(const u32x4*)(Kc + (krow0 + min(k0 + key, max_key)) * kv_rs + (long)kvh * HD + c * 8);
+  }
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i) {
+    const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
+    const int kf = k0 + c * 8;
+    u32x4 v = *(const u32x4*)(vT + (long)(kvh * HD + dim) * vt_stride + vcol0 + kf);
+    if (kf + 7 > max_key) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ka = kf + 2 * e;
+        uint32_t w = v[e];
+        if (ka > max_key) w &= 0xFFFF0000u;
+        if (ka + 1 > max_key) w &= 0x0000FFFFu;
+        v[e] = w;
+      }
     }
+    st.v[i] = v;
+  }
+}
+
+template <int HD>
+__device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD>& t) {
+  constexpr int NCHK = HD / 8;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i) {
+    const int ch = tid + 256 * i, key = ch / NCHK, c = ch % NCHK;
+    *(u32x4*)(t.k + key * HD + chunk_swz<NCHK>(key, c) * 8) = st.k[i];
+  }
+#pragma unroll
+  for (int i = 0; i < HD / 32; ++i) {
+    const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
+    const int g = c >> 1, q = c & 1;  // 16-key group, which half of it
+    // keys 8c..8c+3 -> chunk 2g (half q); keys 8c+4..8c+7 -> chunk 2g+1 (half q)
+    u32x2 lo, hi;
+    lo[0] = st.v[i][0];
+    lo[1] = st.v[i][1];
+    hi[0] = st.v[i][2];
+    hi[1] = st.v[i][3];
+    *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g) * 8 + q * 4) = lo;
+    *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g + 1) * 8 + q * 4) = hi;
   }
 }
 
 // One 64-key tile of the online softmax for the wave's 32 queries.
 //   qb[ks]: Q^T operand (lane: query lane&31, dims 8*(lane>>5) + 16 ks .. +7)
-//   key_abs0: absolute key index of tile key 0; keys with index > lim are masked.
+//   key_abs0: key index of tile key 0; keys with index > lim are masked.
 template <int HD>
-__device__ __forceinline__ void attn_tile_update(const AttnSmem<HD>& sm, const bf16x8* qb,
+__device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf16x8* qb,
                                                  f32x16* o, float& m, float& l, int key_abs0,
                                                  int lim, float scale_log2) {
+  constexpr int NCHK = HD / 8;
   const int lane = threadIdx.x & 63, h = lane >> 5, lr = lane & 31;
   f32x16 s[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+    const int key = kb * 32 + lr;
 #pragma unroll
     for (int ks = 0; ks < HD / 16; ++ks) {
       const bf16x8 a =
-          as_bf16x8(*(const u32x4*)(sm.k + (kb * 32 + lr) * AttnSmem<HD>::KP + ks * 16 + h * 8));
+          as_bf16x8(*(const u32x4*)(t.k + key * HD + chunk_swz<NCHK>(key, 2 * ks + h) * 8));
       s[kb] = mfma32x32x16(a, qb[ks], s[kb]);
     }
   }
@@ -203,18 +260,12 @@ __device__ __forceinline__ void attn_tile_update(const AttnSmem<HD>& sm, const b
       for (int e = 0; e < 4; ++e)
         pw[e] = pack2bf(s[kb][k2 * 8 + 2 * e], s[kb][k2 * 8 + 2 * e + 1]);
       const bf16x8 pb = as_bf16x8(pw);
-      const int key_lo = kb * 32 + k2 * 16 + 4 * h;
+      const int c = 2 * (kb * 2 + k2) + h;
 #pragma unroll
       for (int db = 0; db < HD / 32; ++db) {
-        const bf16* vrow = sm.vt + (db * 32 + lr) * AttnSmem<HD>::VP;
-        const u32x2 v0 = *(const u32x2*)(vrow + key_lo);
-        const u32x2 v1 = *(const u32x2*)(vrow + key_lo + 8);
-        u32x4 va;
-        va[0] = v0[0];
-        va[1] = v0[1];
-        va[2] = v1[0];
-        va[3] = v1[1];
-        o[db] = mfma32x32x16(as_bf16x8(va), pb, o[db]);
+        const int dim = db * 32 + lr;
+        const bf16x8 va = as_bf16x8(*(const u32x4*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, c) * 8));
+        o[db] = mfma32x32x16(va, pb, o[db]);
       }
     }
 }
@@ -236,17 +287,18 @@ __device__ __forceinline__ void attn_store(const f32x16* o, float l, bf16* out_r
     }
 }
 
-// Prefill work item: (seq_start_row, seq_len, kv head, first item) where items
-// enumerate (query block of 32, head within the group) pairs, query-block major.
+// Prefill work item: (first K-cache row of the sequence, its first V^T
+// column, length, kv head, first item) where items enumerate (query block of
+// 32, head within the group) pairs, query-block major.
 struct PrefillItem {
-  int start, len, kvh, item0;
+  int start, vcol, len, kvh, item0;
 };
 
 template <int HD>
-__global__ __launch_bounds__(256) void attn_prefill_mfma_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
-    bf16* __restrict__ O, const PrefillItem* __restrict__ work, AttnGeom g) {
-  __shared__ AttnSmem<HD> sm;
+__global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ vT,
+    long vt_stride, bf16* __restrict__ O, const PrefillItem* __restrict__ work, AttnGeom g) {
+  __shared__ AttnTile<HD> tiles[2];
   const PrefillItem w = work[blockIdx.x];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, lr = lane & 31;
   const int rep = g.H / g.G;
@@ -255,11 +307,10 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma_kernel(
   const bool active = item < n_items;
   const int qb = active ? item / rep : 0;
   const int head = w.kvh * rep + (active ? item % rep : 0);
-  // last key needed by the workgroup: its largest query block
   const int last_item = min(w.item0 + 3, n_items - 1);
   const int wg_last_q = min(((last_item / rep) + 1) * 32, w.len) - 1;
-  const int q_pos = qb * 32 + lr;            // this lane's query position
-  const int q_row = min(q_pos, w.len - 1);   // clamped row for loads
+  const int q_pos = qb * 32 + lr;
+  const int q_row = min(q_pos, w.len - 1);
   const long kv_rs = (long)g.G * HD;
   bf16x8 qbv[HD / 16];
   {
@@ -274,11 +325,18 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma_kernel(
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m = -INFINITY, l = 0.f;
   const int wave_last_q = min(qb * 32 + 31, w.len - 1);
-  for (int k0 = 0; k0 <= wg_last_q; k0 += AT_KT) {
-    attn_load_tile<HD>(sm, Kc, Vc, kv_rs, w.kvh, w.start, k0, w.len - 1);
-    __syncthreads();
+  const int nt = wg_last_q / AT_KT + 1;
+  AttnStage<HD> st;
+  attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, 0, w.len - 1);
+  attn_lstore<HD>(st, tiles[0]);
+  __syncthreads();
+  for (int it = 0; it < nt; ++it) {
+    const int k0 = it * AT_KT;
+    if (it + 1 < nt)
+      attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, k0 + AT_KT, w.len - 1);
     if (active && k0 <= wave_last_q)
-      attn_tile_update<HD>(sm, qbv, o, m, l, k0, q_pos, g.scale_log2);
+      attn_tile_update<HD>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
+    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
     __syncthreads();
   }
   if (active && q_pos < w.len)
@@ -286,28 +344,30 @@ __global__ __launch_bounds__(256) void attn_prefill_mfma_kernel(
 }
 
 // Decode work item: a group of up to 128/rep consecutive sorted anchors of one
-// sequence and one kv head.
+// sequence, one kv head, and the shared keys [kbeg, kend) of that sequence.
+// The item writes, per row (anchor-major, then head within the group), the
+// partial softmax state: running max m and sum l (log2 domain) and the
+// unnormalised output; attn_decode_combine_kernel merges the items of a group
+// with the anchor's private keys.
 struct DecodeItem {
-  int first, count, kvh, seq_start;
+  int first, count, kvh, krow0, vcol0, kbeg, kend, part;
 };
 
 template <int HD>
-__global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ Vc,
-    const bf16* __restrict__ Kp, const bf16* __restrict__ Vp, long priv_rs, int n_priv,
-    const int* __restrict__ apos, bf16* __restrict__ O, const DecodeItem* __restrict__ work,
-    AttnGeom g) {
-  __shared__ AttnSmem<HD> sm;
+__global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ vT,
+    long vt_stride, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
+    float* __restrict__ part_o, float* __restrict__ part_ml, AttnGeom g) {
+  __shared__ AttnTile<HD> tiles[2];
   const DecodeItem w = work[blockIdx.x];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, lr = lane & 31;
   const int rep = g.H / g.G;
   const int rho = wave * 32 + lr;  // row within the group: anchor-major
   const int a_loc = rho / rep;
   const bool active = a_loc < w.count;
-  const int arow = w.first + (active ? a_loc : 0);  // sorted anchor row
+  const int arow = w.first + (active ? a_loc : 0);
   const int head = w.kvh * rep + rho % rep;
-  const int lim = active ? apos[arow] : -1;
-  const int a_max = apos[w.first + w.count - 1];  // sorted: last is largest
+  const int lim = active ? min(apos[arow], w.kend - 1) : -1;
   const long kv_rs = (long)g.G * HD;
   bf16x8 qbv[HD / 16];
   {
@@ -321,71 +381,125 @@ __global__ __launch_bounds__(256) void attn_decode_mfma_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m = -INFINITY, l = 0.f;
-  // rows of this wave that are active: skip tiles beyond the wave's own max anchor
   int wave_lim = lim;
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) wave_lim = max(wave_lim, __shfl_xor(wave_lim, off));
-  for (int k0 = 0; k0 <= a_max; k0 += AT_KT) {
-    attn_load_tile<HD>(sm, Kc, Vc, kv_rs, w.kvh, w.seq_start, k0, a_max);
-    __syncthreads();
-    if (k0 <= wave_lim) attn_tile_update<HD>(sm, qbv, o, m, l, k0, lim, g.scale_log2);
+  const int nt = (w.kend - w.kbeg + AT_KT - 1) / AT_KT;
+  AttnStage<HD> st;
+  attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg, w.kend - 1);
+  attn_lstore<HD>(st, tiles[0]);
+  __syncthreads();
+  for (int it = 0; it < nt; ++it) {
+    const int k0 = w.kbeg + it * AT_KT;
+    if (it + 1 < nt)
+      attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, k0 + AT_KT,
+                     w.kend - 1);
+    if (k0 <= wave_lim) attn_tile_update<HD>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
+    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
     __syncthreads();
   }
   if (!active) return;
-  // private keys of slots 1..n_priv, in chunks of 16 under the same online
-  // softmax; lane half h holds q dims {8h + 16 ks + e}, the partner the rest.
-  const bf16* kp = Kp + (long)arow * priv_rs + (long)w.kvh * HD;
-  const bf16* vp = Vp + (long)arow * priv_rs + (long)w.kvh * HD;
-  for (int c0 = 0; c0 < n_priv; c0 += 16) {
-    const int cn = min(16, n_priv - c0);
-    float sc[16];
-    float pmax = -INFINITY;
+  const long prow = (long)w.part * 128 + rho;
+  float* po = part_o + prow * HD;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      sc[j] = -INFINITY;
-      if (j < cn) {
-        float dot = 0.f;
+  for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
-        for (int ks = 0; ks < HD / 16; ++ks) {
-          const u32x4 kw = *(const u32x4*)(kp + (long)(c0 + j) * kv_rs + ks * 16 + h * 8);
-          const u32x4 qw = __builtin_bit_cast(u32x4, qbv[ks]);
+    for (int i = 0; i < 4; ++i) {
+      f32x4 v;
+      v[0] = o[db][4 * i];
+      v[1] = o[db][4 * i + 1];
+      v[2] = o[db][4 * i + 2];
+      v[3] = o[db][4 * i + 3];
+      *(f32x4*)(po + db * 32 + 8 * i + 4 * h) = v;
+    }
+  if (h == 0) {
+    part_ml[prow * 2] = m;
+    part_ml[prow * 2 + 1] = l;
+  }
+}
+
+// Group of sorted anchors as the combine kernel sees it.
+struct DecodeGroup {
+  int first, nchunk, part0;  // part index of (kv head 0, chunk 0); kv head g adds g*nchunk
+};
+
+// One wave per (sorted anchor r, query head j): merge the chunk partials of
+// its group with its private keys (slots 1..n_priv) under one softmax, write
+// the attention output.
+template <int HD>
+__global__ __launch_bounds__(256) void attn_decode_combine_kernel(
+    const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
+    long priv_rs, int n_priv, const int* __restrict__ grp_of_row,
+    const DecodeGroup* __restrict__ groups, const float* __restrict__ part_o,
+    const float* __restrict__ part_ml, bf16* __restrict__ O, int n_rows, AttnGeom g) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long item = (long)blockIdx.x * 4 + wave;
+  if (item >= (long)n_rows * g.H) return;  // no barrier in this kernel
+  const int r = (int)(item / g.H), j = (int)(item % g.H);
+  const int rep = g.H / g.G, kvh = j / rep;
+  const DecodeGroup grp = groups[grp_of_row[r]];
+  const int rho = (r - grp.first) * rep + j % rep;
+  const long kv_rs = (long)g.G * HD;
+  constexpr int DPL = HD / 64;  // dims per lane
+  // private scores (log2 domain)
+  float q[DPL];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            dot = fmaf(bf2f((bf16)(qw[e] & 0xFFFFu)), bf2f((bf16)(kw[e] & 0xFFFFu)), dot);
-            dot = fmaf(bf2f((bf16)(qw[e] >> 16)), bf2f((bf16)(kw[e] >> 16)), dot);
-          }
-        }
-        dot += __shfl_xor(dot, 32);
-        sc[j] = dot * g.scale_log2;
-        pmax = fmaxf(pmax, sc[j]);
+  for (int e = 0; e < DPL; ++e) q[e] = bf2f(Q[(long)r * g.H * HD + (long)j * HD + lane + 64 * e]);
+  float sc[16];
+  float mtot = -INFINITY;
+  for (int c = 0; c < grp.nchunk; ++c) {
+    const long prow = (long)(grp.part0 + kvh * grp.nchunk + c) * 128 + rho;
+    mtot = fmaxf(mtot, part_ml[prow * 2]);
+  }
+  const bf16* kp = Kp + (long)r * priv_rs + (long)kvh * HD;
+  const bf16* vp = Vp + (long)r * priv_rs + (long)kvh * HD;
+  float acc[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+  float ltot = 0.f;
+  // private keys in chunks of 16 scores
+  for (int t0 = 0; t0 < n_priv; t0 += 16) {
+    const int tn = min(16, n_priv - t0);
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      sc[t] = -INFINITY;
+      if (t < tn) {
+        float d = 0.f;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) d = fmaf(q[e], bf2f(kp[(long)(t0 + t) * kv_rs + lane + 64 * e]), d);
+        sc[t] = wave_sum(d) * g.scale_log2;
       }
     }
-    const float m_new = fmaxf(m, pmax);
-    const float alpha = exp2f(m - m_new);
+    float cm = mtot;
 #pragma unroll
-    for (int db = 0; db < HD / 32; ++db)
+    for (int t = 0; t < 16; ++t) cm = fmaxf(cm, sc[t]);
+    if (cm > mtot) {  // rescale what was accumulated so far (private part only)
+      const float a = exp2f(mtot - cm);
+      ltot *= a;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-    float psum = 0.f;
-    for (int j = 0; j < cn; ++j) {
-      const float p = exp2f(sc[j] - m_new);
-      psum += p;
-      const bf16* vj = vp + (long)(c0 + j) * kv_rs;
-#pragma unroll
-      for (int db = 0; db < HD / 32; ++db)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const u32x2 vv = *(const u32x2*)(vj + db * 32 + 8 * i + 4 * h);
-          o[db][4 * i] = fmaf(p, bf2f((bf16)(vv[0] & 0xFFFFu)), o[db][4 * i]);
-          o[db][4 * i + 1] = fmaf(p, bf2f((bf16)(vv[0] >> 16)), o[db][4 * i + 1]);
-          o[db][4 * i + 2] = fmaf(p, bf2f((bf16)(vv[1] & 0xFFFFu)), o[db][4 * i + 2]);
-          o[db][4 * i + 3] = fmaf(p, bf2f((bf16)(vv[1] >> 16)), o[db][4 * i + 3]);
-        }
+      for (int e = 0; e < DPL; ++e) acc[e] *= a;
+      mtot = cm;
     }
-    l = l * alpha + psum;
-    m = m_new;
+    for (int t = 0; t < tn; ++t) {
+      const float p = exp2f(sc[t] - mtot);
+      ltot += p;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[e] = fmaf(p, bf2f(vp[(long)(t0 + t) * kv_rs + lane + 64 * e]), acc[e]);
+    }
   }
-  attn_store<HD>(o, l, O + (long)arow * g.H * HD + (long)head * HD);
+  for (int c = 0; c < grp.nchunk; ++c) {
+    const long prow = (long)(grp.part0 + kvh * grp.nchunk + c) * 128 + rho;
+    const float mc = part_ml[prow * 2];
+    if (mc == -INFINITY) continue;
+    const float a = exp2f(mc - mtot);
+    ltot = fmaf(part_ml[prow * 2 + 1], a, ltot);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = fmaf(part_o[prow * HD + lane + 64 * e], a, acc[e]);
+  }
+  const float inv = 1.f / ltot;
+  bf16* out = O + (long)r * g.H * HD + (long)j * HD;
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) out[lane + 64 * e] = f2bf(acc[e] * inv);
 }
 
 }  // namespace alr

@@ -24,8 +24,10 @@ template <typename OutT>
 struct EpiQKV {
   OutT* q;            // [M, H*hd]
   OutT* k;            // row r -> k + r*kv_rs
-  OutT* v;            // row r -> v + r*kv_rs
+  OutT* v;            // row r -> v + r*kv_rs (when vt_col is null)
   long kv_rs;
+  const int* vt_col;  // if set: v is transposed, element (row, c) at v[c*vt_stride + vt_col[row]]
+  long vt_stride;
   const float* cosT;  // [max_pos, hd/2]
   const float* sinT;
   const int* pos;     // position of row r is pos[r] + pos_add
@@ -50,6 +52,10 @@ struct EpiQKV {
       const float cs = cosT[p * half + i], sn = sinT[p * half + i];
       Elt<OutT>::st(dst + head * hd + i, lo * cs - hi * sn);
       Elt<OutT>::st(dst + head * hd + i + half, hi * cs + lo * sn);
+    } else if (vt_col) {
+      const long cl = c - qd - kd, col = vt_col[row];
+      Elt<OutT>::st(v + cl * vt_stride + col, lo);
+      Elt<OutT>::st(v + (cl + 32) * vt_stride + col, hi);
     } else {
       OutT* dst = v + (long)row * kv_rs;
       const int cl = c - qd - kd;

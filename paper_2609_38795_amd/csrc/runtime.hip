@@ -44,12 +44,14 @@ struct Layout {
   size_t l_anorm, l_fnorm, l_qkv, l_o, l_gu, l_down;  // offsets within a layer block
   size_t rope_cos, rope_sin;
   size_t kc, vc, kv_layer_stride;
+  size_t vt_stride;  // columns of the transposed V cache (0 when V is stored natural)
   size_t kp, vp, kvp_layer_stride;
   size_t feat_store, hf_store;
   size_t resid, xnorm, qbuf, attn, act;
   size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_cur;
-  size_t i_pwork, i_dwork, i_maps;
-  size_t max_pwork, max_dwork;
+  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow;
+  size_t part_o, part_ml;
+  size_t max_pwork, max_dwork, max_groups;
   size_t total;
 };
 
@@ -110,6 +112,10 @@ alr_status check_limits(const alr_limits* l, char* msg, size_t len) {
 
 int anchor_group(const alr_config& c) { return std::max(1, 128 / (c.n_heads / c.n_kv_heads)); }
 
+bool mfma_attn(const alr_config& c) {
+  return c.dtype == ALR_BF16 && (c.head_dim == 64 || c.head_dim == 128);
+}
+
 size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   const size_t es = (c.dtype == ALR_BF16) ? 2 : 4;
   const size_t d = c.d_model, F = c.d_ffn, V = c.vocab, H = c.n_heads, G = c.n_kv_heads,
@@ -146,7 +152,10 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.layer0 = take(nl * L.layer_stride);
   L.rope_cos = take((size_t)c.max_pos * (hd / 2) * 4);
   L.rope_sin = take((size_t)c.max_pos * (hd / 2) * 4);
-  L.kv_layer_stride = align256(T * kvd * es);
+  // transposed V (MFMA attention): [G*hd][vt_stride] per layer, every sequence
+  // starting at a multiple of 64 columns
+  L.vt_stride = mfma_attn(c) ? ((T + 64 * (size_t)lim.max_seqs + 63) / 64) * 64 : 0;
+  L.kv_layer_stride = align256(std::max(T, L.vt_stride) * kvd * es);
   L.kc = take(nl * L.kv_layer_stride);
   L.vc = take(nl * L.kv_layer_stride);
   L.kvp_layer_stride = align256(NA * np * kvd * es);
@@ -167,10 +176,18 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_aseq = take(NA * 4);
   L.i_cur = take(NA * 4);
   L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
-  L.max_dwork = (NA + std::min<size_t>(lim.max_seqs, NA)) * G;
+  const size_t ag = (size_t)anchor_group(c);
+  L.max_groups = (NA + ag - 1) / ag + std::min<size_t>(lim.max_seqs, NA);
+  const size_t max_chunks = ((size_t)c.max_pos + AT_DECODE_CHUNK - 1) / AT_DECODE_CHUNK;
+  L.max_dwork = mfma_attn(c) ? L.max_groups * G * max_chunks : 0;
   L.i_pwork = take(L.max_pwork * sizeof(PrefillItem));
   L.i_dwork = take(L.max_dwork * sizeof(DecodeItem));
   L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
+  L.i_vtcol = take(T * 4);
+  L.i_groups = take(L.max_groups * sizeof(DecodeGroup));
+  L.i_grprow = take(NA * 4);
+  L.part_o = take(L.max_dwork * 128 * hd * 4);
+  L.part_ml = take(L.max_dwork * 128 * 2 * 4);
   L.total = off;
   return off;
 }
@@ -234,10 +251,12 @@ struct alr_ctx {
   bool prefilled = false;
   int n_seq = 0;
   std::vector<int> seq_len, seq_off;
-  std::vector<int> h_tokpos, h_rowstart;
+  std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
   std::vector<PrefillItem> h_pwork;
   std::vector<int> h_anch;  // perm | apos | atok | aseq, each n_anchor long
   std::vector<DecodeItem> h_dwork;
+  std::vector<DecodeGroup> h_groups;
+  std::vector<int> h_grprow;
   std::string err;
   // launch timing of one site (alr_profile_*)
   int prof_site = 0;
@@ -339,10 +358,6 @@ AttnGeom geom(const alr_config& c) {
   return g;
 }
 
-bool mfma_attn(const alr_config& c) {
-  return c.dtype == ALR_BF16 && (c.head_dim == 64 || c.head_dim == 128);
-}
-
 // Column arrangement of the fused QKV weight: for q (n heads of hd), the
 // original row feeding fused row (64 t + w) -- see EpiQKV.
 void rope_pair_rows(int n, int hd, std::vector<int>& dst_of_src) {
@@ -386,12 +401,18 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
   eq.H = H;
   eq.G = G;
   eq.hd = hd;
+  eq.vt_col = nullptr;
+  eq.vt_stride = 0;
   if (!decode) {
     eq.k = kc;
     eq.v = vc;
     eq.kv_rs = kvd;
     eq.pos = ctx->at<int>(L.i_tokpos);
     eq.pos_add = 0;
+    if (L.vt_stride) {
+      eq.vt_col = ctx->at<int>(L.i_vtcol);
+      eq.vt_stride = (long)L.vt_stride;
+    }
   } else {
     eq.k = kp + (long)(s - 1) * kvd;
     eq.v = vp + (long)(s - 1) * kvd;
@@ -416,9 +437,11 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
       const PrefillItem* wk = ctx->at<PrefillItem>(L.i_pwork);
       if constexpr (std::is_same<T, bf16>::value) {
         if (hd == 128)
-          attn_prefill_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, at, wk, g);
+          attn_prefill_mfma_kernel<128>
+              <<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, at, wk, g);
         else
-          attn_prefill_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, at, wk, g);
+          attn_prefill_mfma_kernel<64>
+              <<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, at, wk, g);
       }
     } else {
       const long items = (long)M * H;
@@ -429,13 +452,23 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
     if (mfma_attn(c)) {
       const int nw = (int)ctx->h_dwork.size();
       const DecodeItem* wk = ctx->at<DecodeItem>(L.i_dwork);
+      float* po = ctx->at<float>(L.part_o);
+      float* pml = ctx->at<float>(L.part_ml);
+      const unsigned ncomb = (unsigned)(((long)M * H + 3) / 4);
+      const int* grow = ctx->at<int>(L.i_grprow);
+      const DecodeGroup* grp = ctx->at<DecodeGroup>(L.i_groups);
       if constexpr (std::is_same<T, bf16>::value) {
-        if (hd == 128)
-          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, kp, vp, priv_rs, s,
-                                                            ctx->at<int>(L.i_apos), at, wk, g);
-        else
-          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, kp, vp, priv_rs, s,
-                                                           ctx->at<int>(L.i_apos), at, wk, g);
+        if (hd == 128) {
+          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(
+              qb, kc, vc, (long)L.vt_stride, ctx->at<int>(L.i_apos), wk, po, pml, g);
+          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(qb, kp, vp, priv_rs, s, grow, grp,
+                                                                 po, pml, at, M, g);
+        } else {
+          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(
+              qb, kc, vc, (long)L.vt_stride, ctx->at<int>(L.i_apos), wk, po, pml, g);
+          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(qb, kp, vp, priv_rs, s, grow, grp,
+                                                                po, pml, at, M, g);
+        }
       }
     } else {
       const long items = (long)M * H;
@@ -745,21 +778,33 @@ alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, cons
   ctx->h_tokpos.resize(M);
   ctx->h_rowstart.resize(M);
   ctx->h_pwork.clear();
+  ctx->h_vtcol.resize(M);
+  ctx->seq_vcol.assign(n_seq, 0);
+  int vcol = 0;
   for (int i = 0; i < n_seq; ++i) {
+    ctx->seq_vcol[i] = vcol;
     for (int p = 0; p < seq_len[i]; ++p) {
       ctx->h_tokpos[ctx->seq_off[i] + p] = p;
       ctx->h_rowstart[ctx->seq_off[i] + p] = ctx->seq_off[i];
+      ctx->h_vtcol[ctx->seq_off[i] + p] = vcol + p;
     }
+    vcol += (seq_len[i] + 63) / 64 * 64;
     const int n_items = ((seq_len[i] + 31) / 32) * rep;
     for (int g = 0; g < c.n_kv_heads; ++g)
       for (int it = 0; it < n_items; it += 4)
-        ctx->h_pwork.push_back(PrefillItem{ctx->seq_off[i], seq_len[i], g, it});
+        ctx->h_pwork.push_back(PrefillItem{ctx->seq_off[i], ctx->seq_vcol[i], seq_len[i], g, it});
   }
+  // causal work grows with the query position: start the longest items first
+  std::stable_sort(ctx->h_pwork.begin(), ctx->h_pwork.end(),
+                   [rep](const PrefillItem& a, const PrefillItem& b) {
+                     return a.item0 / rep > b.item0 / rep;
+                   });
   if (ctx->h_pwork.size() > ctx->L.max_pwork)
     return fail(ctx, ALR_E_WORKSPACE, "prefill work list overflow");
   const Layout& L = ctx->L;
   st = upload(ctx, ctx->at<int>(L.i_tokpos), ctx->h_tokpos.data(), (size_t)M * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_rowstart), ctx->h_rowstart.data(), (size_t)M * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_vtcol), ctx->h_vtcol.data(), (size_t)M * 4, s);
   if (st == ALR_OK)
     st = upload(ctx, ctx->at<PrefillItem>(L.i_pwork), ctx->h_pwork.data(),
                 ctx->h_pwork.size() * sizeof(PrefillItem), s);
@@ -805,18 +850,36 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
     aseq[r] = ctx->seq_off[anchor_seq[i]];
   }
   ctx->h_dwork.clear();
-  const int ag = anchor_group(c);
-  for (int r0 = 0; r0 < n;) {
-    int r1 = r0;
-    while (r1 < n && anchor_seq[order[r1]] == anchor_seq[order[r0]]) ++r1;
-    for (int f = r0; f < r1; f += ag) {
-      const int cnt = std::min(ag, r1 - f);
-      for (int g = 0; g < c.n_kv_heads; ++g)
-        ctx->h_dwork.push_back(DecodeItem{f, cnt, g, aseq[f]});
+  ctx->h_groups.clear();
+  ctx->h_grprow.assign(n, 0);
+  if (mfma_attn(c)) {
+    // groups of up to 128/rep sorted anchors of one sequence; each group x kv
+    // head x 512-key chunk of its shared prefix is one work item
+    const int ag = anchor_group(c);
+    for (int r0 = 0; r0 < n;) {
+      const int sq = anchor_seq[order[r0]];
+      int r1 = r0;
+      while (r1 < n && anchor_seq[order[r1]] == sq) ++r1;
+      for (int f = r0; f < r1; f += ag) {
+        const int cnt = std::min(ag, r1 - f);
+        const int a_max = apos[f + cnt - 1];
+        const int nchunk = (a_max + AT_DECODE_CHUNK) / AT_DECODE_CHUNK;
+        const int gi = (int)ctx->h_groups.size();
+        const int part0 = (int)ctx->h_dwork.size();
+        ctx->h_groups.push_back(DecodeGroup{f, nchunk, part0});
+        for (int rr = f; rr < f + cnt; ++rr) ctx->h_grprow[rr] = gi;
+        for (int g = 0; g < c.n_kv_heads; ++g)
+          for (int ch = 0; ch < nchunk; ++ch) {
+            const int kb = ch * AT_DECODE_CHUNK;
+            const int ke = std::min(a_max + 1, kb + AT_DECODE_CHUNK);
+            ctx->h_dwork.push_back(DecodeItem{f, cnt, g, ctx->seq_off[sq], ctx->seq_vcol[sq], kb,
+                                              ke, (int)ctx->h_dwork.size()});
+          }
+      }
+      r0 = r1;
     }
-    r0 = r1;
   }
-  if (ctx->h_dwork.size() > ctx->L.max_dwork)
+  if (ctx->h_dwork.size() > ctx->L.max_dwork || ctx->h_groups.size() > ctx->L.max_groups)
     return fail(ctx, ALR_E_WORKSPACE, "decode work list overflow");
   const Layout& L = ctx->L;
   // perm, apos, atok, aseq live in consecutive workspace arrays of max_anchors each
@@ -827,6 +890,10 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
   if (st == ALR_OK)
     st = upload(ctx, ctx->at<DecodeItem>(L.i_dwork), ctx->h_dwork.data(),
                 ctx->h_dwork.size() * sizeof(DecodeItem), s);
+  if (st == ALR_OK)
+    st = upload(ctx, ctx->at<DecodeGroup>(L.i_groups), ctx->h_groups.data(),
+                ctx->h_groups.size() * sizeof(DecodeGroup), s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_grprow), ctx->h_grprow.data(), (size_t)n * 4, s);
   if (st != ALR_OK) return st;
   return (c.dtype == ALR_BF16)
              ? rollout_impl<bf16>(ctx, n, block, forced, tokens_out, logprobs_out, feats_out, s)
