@@ -39,7 +39,8 @@ typedef enum {
   ALR_PROF_DECODE_DOWN = 10,
   ALR_PROF_LM_GEMM = 11,      /* output-head GEMM (logits into the caller's rows)   */
   ALR_PROF_LM_FINALIZE = 12,  /* log-sum-exp, greedy argmax, in-place log-softmax   */
-  ALR_PROF_COUNT = 13
+  ALR_PROF_DECODE_COMBINE = 13, /* merge of decode-attention chunk partials (bf16)  */
+  ALR_PROF_COUNT = 14
 } alr_prof_site;
 
 /* Start timing every launch at `site` with HIP events recorded on the launch

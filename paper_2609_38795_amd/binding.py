@@ -258,7 +258,7 @@ class Engine:
 
 PROF_SITES = {"prefill_qkv": 1, "prefill_attn": 2, "prefill_o": 3, "prefill_gu": 4,
               "prefill_down": 5, "decode_qkv": 6, "decode_attn": 7, "decode_o": 8, "decode_gu": 9,
-              "decode_down": 10, "lm_gemm": 11, "lm_finalize": 12}
+              "decode_down": 10, "lm_gemm": 11, "lm_finalize": 12, "decode_combine": 13}
 
 
 def profile_start(eng: "Engine", site: str, capacity: int = 4096):

@@ -70,8 +70,8 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
       sc = dot * g.scale_log2;
     }
     const float m_new = fmaxf(m, wave_max(sc));
-    const float alpha = exp2f(m - m_new);
-    const float p = (j < n_total) ? exp2f(sc - m_new) : 0.f;
+    const float alpha = fast_exp2(m - m_new);
+    const float p = (j < n_total) ? fast_exp2(sc - m_new) : 0.f;
     l = l * alpha + wave_sum(p);
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] *= alpha;
@@ -201,8 +201,11 @@ __device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD
 
 // One 64-key tile of the online softmax for the wave's 32 queries.
 //   qb[ks]: Q^T operand (lane: query lane&31, dims 8*(lane>>5) + 16 ks .. +7)
-//   key_abs0: key index of tile key 0; keys with index > lim are masked.
-template <int HD>
+//   key_abs0: key index of tile key 0; with MASK, keys with index > lim are
+//   masked (tiles entirely at or below every lane's lim skip the masking).
+//   m is the running max of the raw scores; scale_log2 = log2(e)/sqrt(hd) is
+//   applied inside the exponent.
+template <int HD, bool MASK>
 __device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf16x8* qb,
                                                  f32x16* o, float& m, float& l, int key_abs0,
                                                  int lim, float scale_log2) {
@@ -226,31 +229,35 @@ __device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int key = key_abs0 + kb * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-      const float v = (key <= lim) ? s[kb][r] * scale_log2 : -INFINITY;
-      s[kb][r] = v;
-      tmax = fmaxf(tmax, v);
+      if constexpr (MASK) {
+        const int key = key_abs0 + kb * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (key > lim) s[kb][r] = -INFINITY;
+      }
+      tmax = fmaxf(tmax, s[kb][r]);
     }
   tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
   const float m_new = fmaxf(m, tmax);
-  const float mref = (m_new == -INFINITY) ? 0.f : m_new;
-  const float alpha = exp2f(m - mref);
+  const float mref = (m_new == -INFINITY) ? 0.f : m_new * scale_log2;
+  const bool grew = m_new > m;
+  const float alpha = grew ? fast_exp2(m * scale_log2 - mref) : 1.f;
   float psum = 0.f;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float p = exp2f(s[kb][r] - mref);
+      const float p = fast_exp2(fmaf(s[kb][r], scale_log2, -mref));
       s[kb][r] = p;
       psum += p;
     }
   psum += __shfl_xor(psum, 32);
   l = l * alpha + psum;
   m = m_new;
+  if (__any(grew)) {
 #pragma unroll
-  for (int db = 0; db < HD / 32; ++db)
+    for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+  }
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -334,8 +341,12 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
     const int k0 = it * AT_KT;
     if (it + 1 < nt)
       attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, k0 + AT_KT, w.len - 1);
-    if (active && k0 <= wave_last_q)
-      attn_tile_update<HD>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
+    if (active && k0 <= wave_last_q) {
+      if (k0 + AT_KT - 1 > qb * 32)  // some key of the tile lies beyond some query: mask
+        attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
+      else
+        attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
+    }
     if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
     __syncthreads();
   }
@@ -348,15 +359,16 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
 // The item writes, per row (anchor-major, then head within the group), the
 // partial softmax state: running max m and sum l (log2 domain) and the
 // unnormalised output; attn_decode_combine_kernel merges the items of a group
-// with the anchor's private keys.
+// (the item holding the final chunk also folds in the anchor's private keys).
 struct DecodeItem {
-  int first, count, kvh, krow0, vcol0, kbeg, kend, part;
+  int first, count, kvh, krow0, vcol0, kbeg, kend, part, last;  // last: final chunk of the group
 };
 
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ vT,
-    long vt_stride, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
+    long vt_stride, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp, long priv_rs,
+    int n_priv, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
     float* __restrict__ part_o, float* __restrict__ part_ml, AttnGeom g) {
   __shared__ AttnTile<HD> tiles[2];
   const DecodeItem w = work[blockIdx.x];
@@ -381,9 +393,12 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m = -INFINITY, l = 0.f;
-  int wave_lim = lim;
+  int wave_lim = lim, wave_min = active ? lim : 0x7FFFFFFF;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) wave_lim = max(wave_lim, __shfl_xor(wave_lim, off));
+  for (int off = 32; off > 0; off >>= 1) {
+    wave_lim = max(wave_lim, __shfl_xor(wave_lim, off));
+    wave_min = min(wave_min, __shfl_xor(wave_min, off));
+  }
   const int nt = (w.kend - w.kbeg + AT_KT - 1) / AT_KT;
   AttnStage<HD> st;
   attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg, w.kend - 1);
@@ -394,11 +409,72 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     if (it + 1 < nt)
       attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, k0 + AT_KT,
                      w.kend - 1);
-    if (k0 <= wave_lim) attn_tile_update<HD>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
+    if (k0 <= wave_lim) {
+      if (k0 + AT_KT - 1 > wave_min)
+        attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
+      else
+        attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
+    }
     if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
     __syncthreads();
   }
   if (!active) return;
+  if (w.last) {
+    // the anchor's private keys of slots 1..n_priv join the last chunk's softmax;
+    // lane half h holds q dims {8h + 16 ks + e}, the partner lane the rest
+    const bf16* kp = Kp + (long)arow * priv_rs + (long)w.kvh * HD;
+    const bf16* vp = Vp + (long)arow * priv_rs + (long)w.kvh * HD;
+    for (int c0 = 0; c0 < n_priv; c0 += 16) {
+      const int cn = min(16, n_priv - c0);
+      float sc[16];
+      float pmax = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        sc[j] = -INFINITY;
+        if (j < cn) {
+          float dot = 0.f;
+#pragma unroll
+          for (int ks = 0; ks < HD / 16; ++ks) {
+            const u32x4 kw = *(const u32x4*)(kp + (long)(c0 + j) * kv_rs + ks * 16 + h * 8);
+            const u32x4 qw = __builtin_bit_cast(u32x4, qbv[ks]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              dot = fmaf(bf2f((bf16)(qw[e] & 0xFFFFu)), bf2f((bf16)(kw[e] & 0xFFFFu)), dot);
+              dot = fmaf(bf2f((bf16)(qw[e] >> 16)), bf2f((bf16)(kw[e] >> 16)), dot);
+            }
+          }
+          dot += __shfl_xor(dot, 32);
+          sc[j] = dot;  // raw score, like m
+          pmax = fmaxf(pmax, sc[j]);
+        }
+      }
+      const float m_new = fmaxf(m, pmax);
+      const float mref = m_new * g.scale_log2;
+      const float alpha = fast_exp2(m * g.scale_log2 - mref);
+#pragma unroll
+      for (int db = 0; db < HD / 32; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      float psum = 0.f;
+      for (int j = 0; j < cn; ++j) {
+        const float p = fast_exp2(fmaf(sc[j], g.scale_log2, -mref));
+        psum += p;
+        const bf16* vj = vp + (long)(c0 + j) * kv_rs;
+#pragma unroll
+        for (int db = 0; db < HD / 32; ++db)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const u32x2 vv = *(const u32x2*)(vj + db * 32 + 8 * i + 4 * h);
+            o[db][4 * i] = fmaf(p, bf2f((bf16)(vv[0] & 0xFFFFu)), o[db][4 * i]);
+            o[db][4 * i + 1] = fmaf(p, bf2f((bf16)(vv[0] >> 16)), o[db][4 * i + 1]);
+            o[db][4 * i + 2] = fmaf(p, bf2f((bf16)(vv[1] & 0xFFFFu)), o[db][4 * i + 2]);
+            o[db][4 * i + 3] = fmaf(p, bf2f((bf16)(vv[1] >> 16)), o[db][4 * i + 3]);
+          }
+      }
+      l = l * alpha + psum;
+      m = m_new;
+    }
+  }
   const long prow = (long)w.part * 128 + rho;
   float* po = part_o + prow * HD;
 #pragma unroll
@@ -413,7 +489,7 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
       *(f32x4*)(po + db * 32 + 8 * i + 4 * h) = v;
     }
   if (h == 0) {
-    part_ml[prow * 2] = m;
+    part_ml[prow * 2] = m * g.scale_log2;  // log2 domain for the combine
     part_ml[prow * 2 + 1] = l;
   }
 }
@@ -424,14 +500,14 @@ struct DecodeGroup {
 };
 
 // One wave per (sorted anchor r, query head j): merge the chunk partials of
-// its group with its private keys (slots 1..n_priv) under one softmax, write
-// the attention output.
+// its group (log2-domain max m, sum l, unnormalised output) into the
+// attention output.  Lanes own dims lane + 64 e; the loads of different
+// chunks are independent, so they are issued together.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_decode_combine_kernel(
-    const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
-    long priv_rs, int n_priv, const int* __restrict__ grp_of_row,
-    const DecodeGroup* __restrict__ groups, const float* __restrict__ part_o,
-    const float* __restrict__ part_ml, bf16* __restrict__ O, int n_rows, AttnGeom g) {
+    const int* __restrict__ grp_of_row, const DecodeGroup* __restrict__ groups,
+    const float* __restrict__ part_o, const float* __restrict__ part_ml, bf16* __restrict__ O,
+    int n_rows, AttnGeom g) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const long item = (long)blockIdx.x * 4 + wave;
   if (item >= (long)n_rows * g.H) return;  // no barrier in this kernel
@@ -439,59 +515,23 @@ __global__ __launch_bounds__(256) void attn_decode_combine_kernel(
   const int rep = g.H / g.G, kvh = j / rep;
   const DecodeGroup grp = groups[grp_of_row[r]];
   const int rho = (r - grp.first) * rep + j % rep;
-  const long kv_rs = (long)g.G * HD;
   constexpr int DPL = HD / 64;  // dims per lane
-  // private scores (log2 domain)
-  float q[DPL];
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) q[e] = bf2f(Q[(long)r * g.H * HD + (long)j * HD + lane + 64 * e]);
-  float sc[16];
+  const long p0 = (long)(grp.part0 + kvh * grp.nchunk) * 128 + rho;  // chunk c adds c*128
+  // chunk maxima: lane c reads chunk c's m (nchunk <= 64 per pass)
   float mtot = -INFINITY;
-  for (int c = 0; c < grp.nchunk; ++c) {
-    const long prow = (long)(grp.part0 + kvh * grp.nchunk + c) * 128 + rho;
-    mtot = fmaxf(mtot, part_ml[prow * 2]);
+  for (int c0 = 0; c0 < grp.nchunk; c0 += 64) {
+    const int c = c0 + lane;
+    const float mc = (c < grp.nchunk) ? part_ml[(p0 + (long)c * 128) * 2] : -INFINITY;
+    mtot = fmaxf(mtot, wave_max(mc));
   }
-  const bf16* kp = Kp + (long)r * priv_rs + (long)kvh * HD;
-  const bf16* vp = Vp + (long)r * priv_rs + (long)kvh * HD;
-  float acc[DPL];
+  float ltot = 0.f, acc[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-  float ltot = 0.f;
-  // private keys in chunks of 16 scores
-  for (int t0 = 0; t0 < n_priv; t0 += 16) {
-    const int tn = min(16, n_priv - t0);
-#pragma unroll
-    for (int t = 0; t < 16; ++t) {
-      sc[t] = -INFINITY;
-      if (t < tn) {
-        float d = 0.f;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) d = fmaf(q[e], bf2f(kp[(long)(t0 + t) * kv_rs + lane + 64 * e]), d);
-        sc[t] = wave_sum(d) * g.scale_log2;
-      }
-    }
-    float cm = mtot;
-#pragma unroll
-    for (int t = 0; t < 16; ++t) cm = fmaxf(cm, sc[t]);
-    if (cm > mtot) {  // rescale what was accumulated so far (private part only)
-      const float a = exp2f(mtot - cm);
-      ltot *= a;
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] *= a;
-      mtot = cm;
-    }
-    for (int t = 0; t < tn; ++t) {
-      const float p = exp2f(sc[t] - mtot);
-      ltot += p;
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] = fmaf(p, bf2f(vp[(long)(t0 + t) * kv_rs + lane + 64 * e]), acc[e]);
-    }
-  }
+#pragma unroll 4
   for (int c = 0; c < grp.nchunk; ++c) {
-    const long prow = (long)(grp.part0 + kvh * grp.nchunk + c) * 128 + rho;
+    const long prow = p0 + (long)c * 128;
     const float mc = part_ml[prow * 2];
-    if (mc == -INFINITY) continue;
-    const float a = exp2f(mc - mtot);
+    const float a = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mtot);
     ltot = fmaf(part_ml[prow * 2 + 1], a, ltot);
 #pragma unroll
     for (int e = 0; e < DPL; ++e) acc[e] = fmaf(part_o[prow * HD + lane + 64 * e], a, acc[e]);

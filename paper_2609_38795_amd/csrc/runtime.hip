@@ -459,15 +459,17 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
       const DecodeGroup* grp = ctx->at<DecodeGroup>(L.i_groups);
       if constexpr (std::is_same<T, bf16>::value) {
         if (hd == 128) {
-          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(
-              qb, kc, vc, (long)L.vt_stride, ctx->at<int>(L.i_apos), wk, po, pml, g);
-          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(qb, kp, vp, priv_rs, s, grow, grp,
-                                                                 po, pml, at, M, g);
+          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, kp, vp,
+                                                            priv_rs, s, ctx->at<int>(L.i_apos), wk,
+                                                            po, pml, g);
+          ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
+          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, at, M, g);
         } else {
-          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(
-              qb, kc, vc, (long)L.vt_stride, ctx->at<int>(L.i_apos), wk, po, pml, g);
-          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(qb, kp, vp, priv_rs, s, grow, grp,
-                                                                po, pml, at, M, g);
+          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, kp, vp,
+                                                           priv_rs, s, ctx->at<int>(L.i_apos), wk,
+                                                           po, pml, g);
+          ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
+          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, at, M, g);
         }
       }
     } else {
@@ -873,7 +875,7 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
             const int kb = ch * AT_DECODE_CHUNK;
             const int ke = std::min(a_max + 1, kb + AT_DECODE_CHUNK);
             ctx->h_dwork.push_back(DecodeItem{f, cnt, g, ctx->seq_off[sq], ctx->seq_vcol[sq], kb,
-                                              ke, (int)ctx->h_dwork.size()});
+                                              ke, (int)ctx->h_dwork.size(), ch == nchunk - 1});
           }
       }
       r0 = r1;
