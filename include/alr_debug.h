@@ -18,12 +18,18 @@ extern "C" {
 
 /* C[M,N] (fp32, row-major) = A[M,K] * W[N,K]^T, on the library's GEMM kernel
  * for `dtype` (ALR_BF16: bf16 MFMA with fp32 accumulation; ALR_F32: fp32 FMA).
- * All pointers are device pointers, row-major and contiguous; N and K must be
+ * A, W, C are device pointers, row-major and contiguous; N and K must be
  * multiples of 64 (ALR_E_UNSUPPORTED otherwise).  `tile` picks the bf16
- * workgroup tile: 0 = the library's choice for this shape, 1 = 256x128,
- * 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves), 5 = 256x256 (4 waves).  Enqueued on `stream`. */
+ * kernel: 0 = the library's choice for this shape; W read from registers
+ * (pre-shuffled): 6 = 256x256 (8 waves), 7 = 128x128, 8 = 256x128; W staged
+ * through LDS: 1 = 256x128, 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves),
+ * 5 = 256x256 (4 waves).  Tiles 6..8 need a device scratch buffer of
+ * N*K*2 + N*8 bytes (ALR_E_WORKSPACE otherwise) to hold the pre-shuffled W;
+ * the call then synchronises `stream` once after shuffling.  Enqueued on
+ * `stream`. */
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
-                          int32_t N, int32_t K, int32_t tile, alr_stream stream);
+                          int32_t N, int32_t K, int32_t tile, void* scratch,
+                          size_t scratch_bytes, alr_stream stream);
 
 /* Kernel launch sites whose device time can be measured with alr_profile_*. */
 typedef enum {

@@ -93,7 +93,7 @@ def load_library() -> ctypes.CDLL:
     lib.alr_status_string.restype = ctypes.c_char_p
     lib.alr_destroy.argtypes = [vp]
     lib.alr_destroy.restype = None
-    lib.alr_debug_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp]
+    lib.alr_debug_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]
     lib.alr_debug_gemm.restype = ctypes.c_int
     lib.alr_profile_start.argtypes = [vp, i32, i32]
     lib.alr_profile_start.restype = ctypes.c_int
@@ -285,7 +285,13 @@ def debug_gemm(dtype: int, A, W, C, stream=None, tile: int = 0):
     s = stream if stream is not None else torch.cuda.current_stream()
     M, K = A.shape
     N = W.shape[0]
+    scratch = None
+    nbytes = 0
+    if dtype == ALR_BF16 and tile >= 6:
+        nbytes = N * K * 2 + N * 8
+        scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
     st = lib.alr_debug_gemm(dtype, A.data_ptr(), W.data_ptr(), C.data_ptr(), M, N, K, tile,
+                            None if scratch is None else scratch.data_ptr(), nbytes,
                             ctypes.c_void_p(s.cuda_stream))
     if st != 0:
         raise AlrError(st, "alr_debug_gemm")

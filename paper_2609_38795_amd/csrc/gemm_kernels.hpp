@@ -328,6 +328,167 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
   }
 }
 
+// ------------------------------------------------------------------ bf16 MFMA GEMM, W in registers
+//
+// Same contract as gemm_bf16_kernel, but W comes pre-shuffled into the MFMA
+// operand order (see preshuffle_kernel): the fragment of 32 W rows x 16 k
+// that a wave feeds to one 32x32x16 MFMA is one contiguous kilobyte, so each
+// wave streams its W fragments from global memory straight into registers
+// with fully coalesced loads, and only A goes through LDS.  That removes the
+// W half of the LDS traffic, the bound of the LDS-staged kernel (LDS reads
+// 128 bytes per clock per CU).  A fragment register is reloaded with the
+// step two ahead right after the MFMAs that consume it.
+
+// W[N][K] -> Wp: chunk (nb, kb, lane) = W[32 nb + lane % 32][16 kb + 8 (lane / 32) .. +7];
+// the chunk index is (nb * (K/16) + kb) * 64 + lane.  Fused-row permutations
+// are applied on the way: row n of the fused matrix is src[n] (a row pointer).
+__global__ __launch_bounds__(256) void preshuffle_kernel(bf16* __restrict__ dst,
+                                                         const bf16* const* __restrict__ src,
+                                                         int N, int K) {
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;
+  const int KB = K / 16;
+  if (q >= (long)(N / 32) * KB * 64) return;  // N*K/8 chunks of 8 elements
+  const int lane = (int)(q & 63);
+  const long blk = q >> 6;
+  const int kb = (int)(blk % KB), nb = (int)(blk / KB);
+  const int n = nb * 32 + (lane & 31), k = kb * 16 + (lane >> 5) * 8;
+  *(u32x4*)(dst + q * 8) = *(const u32x4*)(src[n] + k);
+}
+
+// Row-major assembly with the same row table: dst row n = src[n] (K elements).
+__global__ __launch_bounds__(256) void gather_rows_ptr_kernel(bf16* __restrict__ dst,
+                                                              const bf16* const* __restrict__ src,
+                                                              int N, int K) {
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;  // 16-byte chunk index
+  const int cpr = K / 8;
+  if (q >= (long)N * cpr) return;
+  const int n = (int)(q / cpr), c = (int)(q % cpr);
+  *(u32x4*)(dst + q * 8) = *(const u32x4*)(src[n] + c * 8);
+}
+
+template <int KS, int NI>
+struct WFrag {
+  bf16x8 b[KS][NI];
+};
+
+template <int TAG, int BM, int BN, int WGM, int WGN, int BK, int OCC, class Epi>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_wd_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ Wp, int M, int N, int K,
+    int tiles_m, int tiles_n, Epi epi) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
+  constexpr int MI = WTM / 32, NI = WTN / 32, KS = BK / 16;
+  constexpr int CPR = BK / 8;
+  constexpr int A_CH = BM * CPR / NT;
+  static_assert(A_CH >= 1 && A_CH * NT == BM * CPR, "A tile does not split evenly");
+  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
+
+  int tm, tn;
+  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const int lr = lane & 31, lh = lane >> 5;
+
+  const bf16* a_src[A_CH];
+  int a_off[A_CH];
+#pragma unroll
+  for (int i = 0; i < A_CH; ++i) {
+    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
+    a_src[i] = A + (long)min(m0 + r, M - 1) * lda + c * 8;
+    a_off[i] = swz<BK>(r, c);
+  }
+  const int KB = K / 16, NB = N / 32;
+  const bf16* w_src[NI];
+#pragma unroll
+  for (int ni = 0; ni < NI; ++ni) {
+    const int nb = min((n0 + wn * WTN) / 32 + ni, NB - 1);
+    w_src[ni] = Wp + ((long)nb * KB * 64 + lane) * 8;
+  }
+  const int nk = K / BK;  // even, >= 2
+  auto wload = [&](WFrag<KS, NI>& f, int ks, int kt) {
+    const int kb = min(kt, nk - 1) * KS + ks;
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni) f.b[ks][ni] = as_bf16x8(*(const u32x4*)(w_src[ni] + (long)kb * 512));
+  };
+  const int klast = (nk - 1) * BK;
+
+  GemmRegs<A_CH> ra0, ra1;
+  WFrag<KS, NI> wf0, wf1;
+  gemm_gload(ra0, a_src, 0);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) wload(wf0, ks, 0);
+  gemm_gload(ra1, a_src, BK);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) wload(wf1, ks, 1);
+  gemm_lstore(ra0, As[0], a_off);
+  __syncthreads();
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
+
+  // one stage: MFMAs of A (LDS stage `as`) x W fragments wf (step kt); wf is
+  // refilled with step kt+2; the other A register set goes to the other stage
+  auto stage = [&](const bf16* as, WFrag<KS, NI>& wf, int kt, const GemmRegs<A_CH>& ra_nx,
+                   bf16* as_nx) {
+    bf16x8 af[2][MI];
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+      af[0][mi] = as_bf16x8(*(const u32x4*)(as + swz<BK>(wm * WTM + mi * 32 + lr, lh)));
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int mi = 0; mi < MI; ++mi)
+          af[(ks + 1) & 1][mi] =
+              as_bf16x8(*(const u32x4*)(as + swz<BK>(wm * WTM + mi * 32 + lr, 2 * (ks + 1) + lh)));
+      }
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+          acc[mi][ni] = mfma32x32x16(af[ks & 1][mi], wf.b[ks][ni], acc[mi][ni]);
+      wload(wf, ks, kt + 2);
+#pragma unroll
+      for (int i = 0; i < A_CH; ++i)
+        if (i % KS == ks) *(u32x4*)(as_nx + a_off[i]) = ra_nx.v[i];
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  for (int kt = 0; kt < nk; kt += 2) {
+    const int k2 = min((kt + 2) * BK, klast), k3 = min((kt + 3) * BK, klast);
+    gemm_gload(ra0, a_src, k2);
+    __builtin_amdgcn_sched_barrier(0);
+    stage(As[0], wf0, kt, ra1, As[1]);
+    __syncthreads();
+    gemm_gload(ra1, a_src, k3);
+    __builtin_amdgcn_sched_barrier(0);
+    stage(As[1], wf1, kt + 1, ra0, As[0]);
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int nj = 0; nj < NI / 2; ++nj) {
+    const int col = n0 + wn * WTN + nj * 64 + lr;
+    if (col < N) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
+        }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32 FMA GEMM
 
 constexpr int GF_M = 64, GF_N = 64, GF_K = 16;

@@ -49,7 +49,7 @@ struct Layout {
   size_t feat_store, hf_store;
   size_t resid, xnorm, qbuf, attn, act;
   size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_cur;
-  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow;
+  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
   size_t max_pwork, max_dwork, max_groups;
   size_t total;
@@ -183,6 +183,7 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_pwork = take(L.max_pwork * sizeof(PrefillItem));
   L.i_dwork = take(L.max_dwork * sizeof(DecodeItem));
   L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
+  L.i_rowptr = take(std::max((size_t)c.vocab, qd + 2 * kvd + 2 * d + 2 * F) * sizeof(void*));
   L.i_vtcol = take(T * 4);
   L.i_groups = take(L.max_groups * sizeof(DecodeGroup));
   L.i_grprow = take(NA * 4);
@@ -317,32 +318,36 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
   if (M <= 0) return;
   ProfScope ps(ctx, TAG, st);
   if constexpr (std::is_same<T, bf16>::value) {
-    // largest tile that still fills the 256 CUs: 256x256 (8 waves) for the
-    // prefill and the wide decode GEMMs, 128x128 otherwise; BK = 64 where K
-    // allows an even number of 64-deep steps
+    // W row-major, staged through LDS: 256x256 with 8 waves for the prefill
+    // and wide decode GEMMs, 128x128 (then 64x128) where that fills the CUs.
+    // force_tile 6..8 (debug hook only) select the W-from-registers kernel,
+    // which needs W pre-shuffled.
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     int cfg = force_tile;
     if (cfg == 0) cfg = tiles(256, 256) >= 256 ? 4 : (tiles(128, 128) >= 256 ? 2 : 3);
     const bool k64 = (K % 128) == 0;
-    const int bm = (cfg == 1 || cfg >= 4) ? 256 : (cfg == 2 ? 128 : 64);
-    const int bn = cfg >= 4 ? 256 : 128;
+    const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8) ? 256 : (cfg == 3 ? 64 : 128);
+    const int bn = (cfg == 4 || cfg == 5 || cfg == 6) ? 256 : 128;
     const int tm = (M + bm - 1) / bm, tn = (N + bn - 1) / bn;
     const int nb = tm * tn;
 #define ALR_GEMM(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                      \
   gemm_bf16_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                          \
       <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
-    if (cfg == 5) {
-      if (k64) ALR_GEMM(256, 256, 2, 2, 64, 1); else ALR_GEMM(256, 256, 2, 2, 32, 1);
-    } else if (cfg == 4) {
-      if (k64) ALR_GEMM(256, 256, 2, 4, 64, 1); else ALR_GEMM(256, 256, 2, 4, 32, 1);
-    } else if (cfg == 1) {
-      if (k64) ALR_GEMM(256, 128, 2, 2, 64, 1); else ALR_GEMM(256, 128, 2, 2, 32, 1);
-    } else if (cfg == 2) {
-      if (k64) ALR_GEMM(128, 128, 2, 2, 64, 2); else ALR_GEMM(128, 128, 2, 2, 32, 2);
-    } else {
-      if (k64) ALR_GEMM(64, 128, 2, 2, 64, 2); else ALR_GEMM(64, 128, 2, 2, 32, 4);
+#define ALR_GEMM_WD(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                   \
+  gemm_bf16_wd_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                       \
+      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, M, N, K, tm, tn, epi)
+    switch (cfg) {
+      case 6: ALR_GEMM_WD(256, 256, 2, 4, 32, 1); break;
+      case 7: ALR_GEMM_WD(128, 128, 2, 2, 32, 2); break;
+      case 8: ALR_GEMM_WD(256, 128, 2, 2, 32, 1); break;
+      case 5: if (k64) ALR_GEMM(256, 256, 2, 2, 64, 1); else ALR_GEMM(256, 256, 2, 2, 32, 1); break;
+      case 4: if (k64) ALR_GEMM(256, 256, 2, 4, 64, 1); else ALR_GEMM(256, 256, 2, 4, 32, 1); break;
+      case 1: if (k64) ALR_GEMM(256, 128, 2, 2, 64, 1); else ALR_GEMM(256, 128, 2, 2, 32, 1); break;
+      case 2: if (k64) ALR_GEMM(128, 128, 2, 2, 64, 2); else ALR_GEMM(128, 128, 2, 2, 32, 2); break;
+      default: if (k64) ALR_GEMM(64, 128, 2, 2, 64, 2); else ALR_GEMM(64, 128, 2, 2, 32, 4); break;
     }
 #undef ALR_GEMM
+#undef ALR_GEMM_WD
   } else {
     const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
     gemm_f32_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
@@ -706,38 +711,86 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
   const int H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
   const size_t qd = (size_t)H * hd, kvd = (size_t)G * hd;
   CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_embed, w->tok_embed, V * d * es, hipMemcpyDeviceToDevice, s));
-  CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_lm, w->lm_head, V * d * es, hipMemcpyDeviceToDevice, s));
   CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_fnorm, w->final_norm, d * es, hipMemcpyDeviceToDevice, s));
 
-  // row maps (uploaded once, shared by all layers)
-  std::vector<int> qmap, kmap, maps;
+  // Fused weight rows: q and k rows are arranged so that every rotate-half
+  // partner sits 32 columns after its pair (rope_pair_rows), gate and up rows
+  // alternate in blocks of 32.  src_of[n] is the source row of fused row n.
+  std::vector<int> qmap, kmap;
   rope_pair_rows(H, hd, qmap);
   rope_pair_rows(G, hd, kmap);
-  maps.reserve(qd + 2 * kvd + 2 * F);
-  for (int x : qmap) maps.push_back(x);
-  for (int x : kmap) maps.push_back((int)qd + x);
-  for (size_t i = 0; i < kvd; ++i) maps.push_back((int)(qd + kvd + i));
-  for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + (i % 32)));       // gate
-  for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + 32 + (i % 32)));  // up
-  int* dmaps = ctx->at<int>(L.i_maps);
-  CREATE_HIP(hipMemcpyAsync(dmaps, maps.data(), maps.size() * 4, hipMemcpyHostToDevice, s));
-  const long rb = (long)d * es;
-  for (int l = 0; l < c.n_layers; ++l) {
-    char* lw = ctx->layer(l);
-    CREATE_HIP(hipMemcpyAsync(lw + L.l_anorm, w->attn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
-    CREATE_HIP(hipMemcpyAsync(lw + L.l_fnorm, w->ffn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
-    scatter_rows_kernel<<<(unsigned)qd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wq[l], dmaps, rb);
-    scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wk[l],
-                                                      dmaps + qd, rb);
-    scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wv[l],
-                                                      dmaps + qd + kvd, rb);
-    CREATE_HIP(hipMemcpyAsync(lw + L.l_o, w->wo[l], d * qd * es, hipMemcpyDeviceToDevice, s));
-    scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_gate[l],
-                                                    dmaps + qd + 2 * kvd, rb);
-    scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_up[l],
-                                                    dmaps + qd + 2 * kvd + F, rb);
-    CREATE_HIP(hipMemcpyAsync(lw + L.l_down, w->w_down[l], d * F * es, hipMemcpyDeviceToDevice, s));
+  std::vector<int> q_src(qd), k_src(kvd);
+  for (size_t i = 0; i < qd; ++i) q_src[qmap[i]] = (int)i;
+  for (size_t i = 0; i < kvd; ++i) k_src[kmap[i]] = (int)i;
+  if (c.dtype == ALR_BF16) {
+    // bf16: fused weights assembled row-major from a table of source rows
+    const size_t qkv = qd + 2 * kvd;
+    std::vector<const bf16*> rp;
+    const void** drp = ctx->at<const void*>(L.i_rowptr);
+    auto shuffle = [&](char* dst, const bf16* const* rows_dev, int N, int K) {
+      const long chunks = (long)N * (K / 8);
+      gather_rows_ptr_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
+          reinterpret_cast<bf16*>(dst), rows_dev, N, K);
+    };
+    rp.resize(V);
+    for (size_t n = 0; n < V; ++n) rp[n] = (const bf16*)w->lm_head + n * d;
+    CREATE_HIP(hipMemcpyAsync(drp, rp.data(), V * sizeof(void*), hipMemcpyHostToDevice, s));
+    shuffle(ctx->ws + L.w_lm, (const bf16* const*)drp, (int)V, (int)d);
     CREATE_HIP(hipGetLastError());
+    CREATE_HIP(hipStreamSynchronize(s));  // the pointer table is rewritten below
+    for (int l = 0; l < c.n_layers; ++l) {
+      char* lw = ctx->layer(l);
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_anorm, w->attn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_fnorm, w->ffn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+      rp.clear();
+      for (size_t n = 0; n < qd; ++n) rp.push_back((const bf16*)w->wq[l] + (size_t)q_src[n] * d);
+      for (size_t n = 0; n < kvd; ++n) rp.push_back((const bf16*)w->wk[l] + (size_t)k_src[n] * d);
+      for (size_t n = 0; n < kvd; ++n) rp.push_back((const bf16*)w->wv[l] + n * d);
+      for (size_t n = 0; n < d; ++n) rp.push_back((const bf16*)w->wo[l] + n * qd);
+      for (size_t n = 0; n < 2 * F; ++n) {
+        const size_t t = n / 64, wi = n % 64;
+        rp.push_back(wi < 32 ? (const bf16*)w->w_gate[l] + (t * 32 + wi) * d
+                             : (const bf16*)w->w_up[l] + (t * 32 + wi - 32) * d);
+      }
+      for (size_t n = 0; n < d; ++n) rp.push_back((const bf16*)w->w_down[l] + n * F);
+      CREATE_HIP(hipMemcpyAsync(drp, rp.data(), rp.size() * sizeof(void*), hipMemcpyHostToDevice, s));
+      const bf16* const* r0 = (const bf16* const*)drp;
+      shuffle(lw + L.l_qkv, r0, (int)qkv, (int)d);
+      shuffle(lw + L.l_o, r0 + qkv, (int)d, (int)qd);
+      shuffle(lw + L.l_gu, r0 + qkv + d, (int)(2 * F), (int)d);
+      shuffle(lw + L.l_down, r0 + qkv + d + 2 * F, (int)d, (int)F);
+      CREATE_HIP(hipGetLastError());
+      CREATE_HIP(hipStreamSynchronize(s));
+    }
+  } else {
+    CREATE_HIP(hipMemcpyAsync(ctx->ws + L.w_lm, w->lm_head, V * d * es, hipMemcpyDeviceToDevice, s));
+    std::vector<int> maps;  // destination row of each source row
+    maps.reserve(qd + 2 * kvd + 2 * F);
+    for (int x : qmap) maps.push_back(x);
+    for (int x : kmap) maps.push_back((int)qd + x);
+    for (size_t i = 0; i < kvd; ++i) maps.push_back((int)(qd + kvd + i));
+    for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + (i % 32)));       // gate
+    for (size_t i = 0; i < F; ++i) maps.push_back((int)((i / 32) * 64 + 32 + (i % 32)));  // up
+    int* dmaps = ctx->at<int>(L.i_maps);
+    CREATE_HIP(hipMemcpyAsync(dmaps, maps.data(), maps.size() * 4, hipMemcpyHostToDevice, s));
+    const long rb = (long)d * es;
+    for (int l = 0; l < c.n_layers; ++l) {
+      char* lw = ctx->layer(l);
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_anorm, w->attn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_fnorm, w->ffn_norm[l], d * es, hipMemcpyDeviceToDevice, s));
+      scatter_rows_kernel<<<(unsigned)qd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wq[l], dmaps, rb);
+      scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wk[l],
+                                                        dmaps + qd, rb);
+      scatter_rows_kernel<<<(unsigned)kvd, 256, 0, s>>>(lw + L.l_qkv, (const char*)w->wv[l],
+                                                        dmaps + qd + kvd, rb);
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_o, w->wo[l], d * qd * es, hipMemcpyDeviceToDevice, s));
+      scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_gate[l],
+                                                      dmaps + qd + 2 * kvd, rb);
+      scatter_rows_kernel<<<(unsigned)F, 256, 0, s>>>(lw + L.l_gu, (const char*)w->w_up[l],
+                                                      dmaps + qd + 2 * kvd + F, rb);
+      CREATE_HIP(hipMemcpyAsync(lw + L.l_down, w->w_down[l], d * F * es, hipMemcpyDeviceToDevice, s));
+      CREATE_HIP(hipGetLastError());
+    }
   }
   // RoPE tables: angles in double, stored as float cos/sin [max_pos, hd/2]
   {
@@ -915,22 +968,40 @@ void alr_destroy(alr_ctx* ctx) {
 // ------------------------------------------------------------------ debug hooks
 
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
-                          int32_t N, int32_t K, int32_t tile, alr_stream stream) {
+                          int32_t N, int32_t K, int32_t tile, void* scratch, size_t scratch_bytes,
+                          alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
+  if (tile < 0 || tile > 8) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
   el.rs = N;
   el.perm = nullptr;
   alr_ctx dummy;
-  if (dtype == ALR_BF16)
-    launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, (const bf16*)W, K, M, N, K, el, s,
-                         tile >= 0 && tile <= 5 ? tile : 0);
-  else if (dtype == ALR_F32)
+  if (dtype == ALR_BF16) {
+    const bf16* Wk = (const bf16*)W;
+    if (tile >= 6) {
+      // the W-from-registers kernel reads W pre-shuffled: shuffle into the scratch buffer
+      const size_t wbytes = (size_t)N * K * 2, need = wbytes + (size_t)N * sizeof(void*);
+      if (!scratch || scratch_bytes < need) return ALR_E_WORKSPACE;
+      std::vector<const bf16*> rp(N);
+      for (int n = 0; n < N; ++n) rp[n] = Wk + (size_t)n * K;
+      const bf16** drp = reinterpret_cast<const bf16**>(static_cast<char*>(scratch) + wbytes);
+      if (hipMemcpyAsync(drp, rp.data(), N * sizeof(void*), hipMemcpyHostToDevice, s) != hipSuccess)
+        return ALR_E_HIP;
+      const long chunks = (long)(N / 32) * (K / 16) * 64;  // N*K/8
+      preshuffle_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
+          static_cast<bf16*>(scratch), drp, N, K);
+      if (hipStreamSynchronize(s) != hipSuccess) return ALR_E_HIP;
+      Wk = static_cast<const bf16*>(scratch);
+    }
+    launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, Wk, K, M, N, K, el, s, tile);
+  } else if (dtype == ALR_F32) {
     launch_gemm<0, float>(&dummy, (const float*)A, K, (const float*)W, K, M, N, K, el, s);
-  else
+  } else {
     return ALR_E_INVALID_ARG;
+  }
   return hipGetLastError() == hipSuccess ? ALR_OK : ALR_E_HIP;
 }
 

@@ -19,10 +19,13 @@ def _print(*a):
 
 
 # ------------------------------------------------------------------ GEMM kernels
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("dtype,tile", [("bf16", 0), ("f32", 0), ("bf16", 1), ("bf16", 2),
+                                        ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 6),
+                                        ("bf16", 7), ("bf16", 8)])
 @pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 192, 256), (1024, 640, 1152)])
-def test_gemm_kernel(dtype, M, N, K):
-    _print(f"gemm {dtype} {M}x{N}x{K}")
+def test_gemm_kernel(dtype, tile, M, N, K):
+    """Every GEMM kernel variant against a float64 product, ragged M and partial N tiles."""
+    _print(f"gemm {dtype} tile {tile} {M}x{N}x{K}")
     rng = np.random.default_rng(M + N + K)
     a = rng.standard_normal((M, K)).astype(np.float32)
     w = rng.standard_normal((N, K)).astype(np.float32)
@@ -36,7 +39,7 @@ def test_gemm_kernel(dtype, M, N, K):
         ta, tw = torch.from_numpy(a).cuda(), torch.from_numpy(w).cuda()
         code = binding.ALR_F32
     c = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    binding.debug_gemm(code, ta, tw, c)
+    binding.debug_gemm(code, ta, tw, c, tile=tile)
     torch.cuda.synchronize()
     ref = a.astype(np.float64) @ w.astype(np.float64).T
     err = np.abs(c.cpu().numpy() - ref).max()
