@@ -23,7 +23,8 @@ extern "C" {
  * kernel: 0 = the library's choice for this shape; W read from registers
  * (pre-shuffled): 6 = 256x256 (8 waves), 7 = 128x128, 8 = 256x128; W staged
  * through LDS: 1 = 256x128, 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves),
- * 5 = 256x256 (4 waves).  Tiles 6..8 need a device scratch buffer of
+ * 5 = 256x256 (4 waves); three-stage LDS ring: 9 = 256x256 (8 waves),
+ * 10 = 128x128.  Tiles 6..8 need a device scratch buffer of
  * N*K*2 + N*8 bytes (ALR_E_WORKSPACE otherwise) to hold the pre-shuffled W;
  * the call then synchronises `stream` once after shuffling.  Enqueued on
  * `stream`. */

@@ -287,7 +287,7 @@ def debug_gemm(dtype: int, A, W, C, stream=None, tile: int = 0):
     N = W.shape[0]
     scratch = None
     nbytes = 0
-    if dtype == ALR_BF16 and tile >= 6:
+    if dtype == ALR_BF16 and 6 <= tile <= 8:
         nbytes = N * K * 2 + N * 8
         scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
     st = lib.alr_debug_gemm(dtype, A.data_ptr(), W.data_ptr(), C.data_ptr(), M, N, K, tile,

@@ -328,6 +328,144 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
   }
 }
 
+// ------------------------------------------------------------------ bf16 MFMA GEMM, 3-stage LDS ring
+//
+// As gemm_bf16_kernel (BK = 32), but with three LDS stages: the operands of
+// step k are written to LDS during step k-2, so when step k-1 ends its
+// fragments are already published and the first k-slice of step k is read
+// before step k-1's barrier -- no wave waits for LDS right after a barrier.
+// Global loads still run one step ahead of the LDS writes (two register sets).
+
+template <int BM, int BN, int MI, int NI, int WTM, int WTN>
+__device__ __forceinline__ void gemm_r3_frag(GemmFrag<MI, NI>& f, const bf16* As, const bf16* Ws,
+                                             int wm, int wn, int ks) {
+  gemm_frag_load<32, MI, NI, WTM, WTN>(f, As, Ws, wm, wn, ks);
+}
+
+template <int TAG, int BM, int BN, int WGM, int WGN, int OCC, class Epi>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_r3_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
+    int tiles_m, int tiles_n, Epi epi) {
+  constexpr int BK = 32, KS = 2, CPR = 4;
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;
+  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
+  constexpr int MI = WTM / 32, NI = WTN / 32;
+  constexpr int A_CH = BM * CPR / NT, W_CH = BN * CPR / NT;
+  static_assert(A_CH >= 1 && W_CH >= 1 && A_CH * NT == BM * CPR && W_CH * NT == BN * CPR,
+                "tile does not split evenly over the threads");
+  constexpr int AS = BM * BK, WS = BN * BK;  // elements per stage
+  __shared__ __attribute__((aligned(16))) bf16 As[3 * AS];
+  __shared__ __attribute__((aligned(16))) bf16 Ws[3 * WS];
+
+  int tm, tn;
+  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  const bf16* a_src[A_CH];
+  const bf16* w_src[W_CH];
+  int a_off[A_CH], w_off[W_CH];
+#pragma unroll
+  for (int i = 0; i < A_CH; ++i) {
+    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
+    a_src[i] = A + (long)min(m0 + r, M - 1) * lda + c * 8;
+    a_off[i] = swz<BK>(r, c);
+  }
+#pragma unroll
+  for (int i = 0; i < W_CH; ++i) {
+    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
+    w_src[i] = W + (long)min(n0 + r, N - 1) * ldw + c * 8;
+    w_off[i] = swz<BK>(r, c);
+  }
+  const int nk = K / BK;  // even, >= 2
+  const int klast = (nk - 1) * BK;
+
+  GemmRegs<A_CH> ra0, ra1;
+  GemmRegs<W_CH> rw0, rw1;
+  // prologue: steps 0 and 1 into LDS stages 0 and 1, step 2 in register set 0
+  gemm_gload(ra0, a_src, 0);
+  gemm_gload(rw0, w_src, 0);
+  gemm_gload(ra1, a_src, BK);
+  gemm_gload(rw1, w_src, BK);
+  gemm_lstore(ra0, As, a_off);
+  gemm_lstore(rw0, Ws, w_off);
+  gemm_gload(ra0, a_src, min(2 * BK, klast));
+  gemm_gload(rw0, w_src, min(2 * BK, klast));
+  gemm_lstore(ra1, As + AS, a_off);
+  gemm_lstore(rw1, Ws + WS, w_off);
+  __syncthreads();
+
+  f32x16 acc[MI][NI];
+#pragma unroll
+  for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
+
+  GemmFrag<MI, NI> f0, f1;
+  gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f0, As, Ws, wm, wn, 0);
+
+  // step kt: compute LDS stage s (= kt mod 3); the register set holding step
+  // kt+2 goes to stage (kt+2) mod 3; the other set is refilled with step kt+3.
+  auto step = [&](int kt, int s, GemmRegs<A_CH>& ra_w, GemmRegs<W_CH>& rw_w,
+                  GemmRegs<A_CH>& ra_l, GemmRegs<W_CH>& rw_l) {
+    const int kn = min((kt + 3) * BK, klast);
+    gemm_gload(ra_l, a_src, kn);
+    gemm_gload(rw_l, w_src, kn);
+    __builtin_amdgcn_sched_barrier(0);
+    const int s1 = (s == 2) ? 0 : s + 1, s2 = (s1 == 2) ? 0 : s1 + 1;
+    const bf16* as = As + s * AS;
+    const bf16* ws = Ws + s * WS;
+    // k-slice 0 (fragments f0 were read earlier), prefetch slice 1
+    gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f1, as, ws, wm, wn, 1);
+    gemm_frag_mma<MI, NI>(f0, acc);
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i)
+      if (i % 2 == 0) *(u32x4*)(As + s2 * AS + a_off[i]) = ra_w.v[i];
+#pragma unroll
+    for (int i = 0; i < W_CH; ++i)
+      if (i % 2 == 0) *(u32x4*)(Ws + s2 * WS + w_off[i]) = rw_w.v[i];
+    __builtin_amdgcn_sched_barrier(0);
+    // k-slice 1; prefetch slice 0 of the next step (its stage is already published)
+    gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f0, As + s1 * AS, Ws + s1 * WS, wm, wn, 0);
+    gemm_frag_mma<MI, NI>(f1, acc);
+#pragma unroll
+    for (int i = 0; i < A_CH; ++i)
+      if (i % 2 == 1) *(u32x4*)(As + s2 * AS + a_off[i]) = ra_w.v[i];
+#pragma unroll
+    for (int i = 0; i < W_CH; ++i)
+      if (i % 2 == 1) *(u32x4*)(Ws + s2 * WS + w_off[i]) = rw_w.v[i];
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+  };
+
+  int s = 0;
+  for (int kt = 0; kt < nk; kt += 2) {
+    step(kt, s, ra0, rw0, ra1, rw1);  // writes step kt+2 (set 0), loads step kt+3 (set 1)
+    s = (s == 2) ? 0 : s + 1;
+    step(kt + 1, s, ra1, rw1, ra0, rw0);  // writes step kt+3 (set 1), loads step kt+4 (set 0)
+    s = (s == 2) ? 0 : s + 1;
+  }
+
+  const int lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int nj = 0; nj < NI / 2; ++nj) {
+    const int col = n0 + wn * WTN + nj * 64 + lr;
+    if (col < N) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
+        }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ bf16 MFMA GEMM, W in registers
 //
 // Same contract as gemm_bf16_kernel, but W comes pre-shuffled into the MFMA

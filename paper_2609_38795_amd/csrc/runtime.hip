@@ -326,17 +326,23 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     int cfg = force_tile;
     if (cfg == 0) cfg = tiles(256, 256) >= 256 ? 4 : (tiles(128, 128) >= 256 ? 2 : 3);
     const bool k64 = (K % 128) == 0;
-    const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8) ? 256 : (cfg == 3 ? 64 : 128);
-    const int bn = (cfg == 4 || cfg == 5 || cfg == 6) ? 256 : 128;
+    const int bm =
+        (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8 || cfg == 9) ? 256 : (cfg == 3 ? 64 : 128);
+    const int bn = (cfg == 4 || cfg == 5 || cfg == 6 || cfg == 9) ? 256 : 128;
     const int tm = (M + bm - 1) / bm, tn = (N + bn - 1) / bn;
     const int nb = tm * tn;
 #define ALR_GEMM(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                      \
   gemm_bf16_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                          \
       <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
+#define ALR_GEMM_R3(BM_, BN_, WGM_, WGN_, OCC_)                                        \
+  gemm_bf16_r3_kernel<TAG, BM_, BN_, WGM_, WGN_, OCC_, Epi>                            \
+      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
 #define ALR_GEMM_WD(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                   \
   gemm_bf16_wd_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                       \
       <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, M, N, K, tm, tn, epi)
     switch (cfg) {
+      case 9: ALR_GEMM_R3(256, 256, 2, 4, 1); break;
+      case 10: ALR_GEMM_R3(128, 128, 2, 2, 2); break;
       case 6: ALR_GEMM_WD(256, 256, 2, 4, 32, 1); break;
       case 7: ALR_GEMM_WD(128, 128, 2, 2, 32, 2); break;
       case 8: ALR_GEMM_WD(256, 128, 2, 2, 32, 1); break;
@@ -347,6 +353,7 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
       default: if (k64) ALR_GEMM(64, 128, 2, 2, 64, 2); else ALR_GEMM(64, 128, 2, 2, 32, 4); break;
     }
 #undef ALR_GEMM
+#undef ALR_GEMM_R3
 #undef ALR_GEMM_WD
   } else {
     const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
@@ -972,7 +979,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || tile > 8) return ALR_E_INVALID_ARG;
+  if (tile < 0 || tile > 10) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
@@ -981,7 +988,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   alr_ctx dummy;
   if (dtype == ALR_BF16) {
     const bf16* Wk = (const bf16*)W;
-    if (tile >= 6) {
+    if (tile >= 6 && tile <= 8) {
       // the W-from-registers kernel reads W pre-shuffled: shuffle into the scratch buffer
       const size_t wbytes = (size_t)N * K * 2, need = wbytes + (size_t)N * sizeof(void*);
       if (!scratch || scratch_bytes < need) return ALR_E_WORKSPACE;
