@@ -24,7 +24,12 @@ extern "C" {
  * (pre-shuffled): 6 = 256x256 (8 waves), 7 = 128x128, 8 = 256x128; W staged
  * through LDS: 1 = 256x128, 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves),
  * 5 = 256x256 (4 waves); three-stage LDS ring: 9 = 256x256 (8 waves),
- * 10 = 128x128.  Tiles 6..8 need a device scratch buffer of
+ * 10 = 128x128; operands loaded straight into an LDS ring (no register
+ * staging): 11 = 256x256 (8 waves, 4 stages), 12 = 256x256 (8 waves,
+ * 5 stages), 13 = 256x256 (4 waves, 4 stages), 14 = 128x128 (4 stages);
+ * ping-pong (the two waves of each SIMD alternate LDS/transfer and MFMA
+ * phases): 15 = 256x256 (4 stages), 16 = 256x256 (5 stages); 17 = ping-pong
+ * over register-staged BK = 64 tiles (K a multiple of 64).  Tiles 6..8 need a device scratch buffer of
  * N*K*2 + N*8 bytes (ALR_E_WORKSPACE otherwise) to hold the pre-shuffled W;
  * the call then synchronises `stream` once after shuffling.  Enqueued on
  * `stream`. */

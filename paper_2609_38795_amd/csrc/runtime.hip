@@ -318,17 +318,25 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
   if (M <= 0) return;
   ProfScope ps(ctx, TAG, st);
   if constexpr (std::is_same<T, bf16>::value) {
-    // W row-major, staged through LDS: 256x256 with 8 waves for the prefill
-    // and wide decode GEMMs, 128x128 (then 64x128) where that fills the CUs.
-    // force_tile 6..8 (debug hook only) select the W-from-registers kernel,
-    // which needs W pre-shuffled.
+    // W row-major.  256x256 ping-pong (BK = 64) for the prefill and wide decode
+    // GEMMs, 128x128 (then 64x128) LDS-staged tiles where 256x256 would leave
+    // CUs idle.  force_tile (debug hook only) picks any variant; 6..8 need W
+    // pre-shuffled.
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     int cfg = force_tile;
-    if (cfg == 0) cfg = tiles(256, 256) >= 256 ? 4 : (tiles(128, 128) >= 256 ? 2 : 3);
+    if (cfg == 0)
+      cfg = tiles(256, 256) >= 256 ? ((K % 64) == 0 ? 17 : 4) : (tiles(128, 128) >= 256 ? 2 : 3);
+    // the direct-to-LDS kernels address operands with 32-bit byte offsets
+    const bool dma_ok = (K % 32) == 0 && ((size_t)(M - 1) * lda + K) * 2 <= 0xFFFFFFFFull &&
+                        ((size_t)(N - 1) * ldw + K) * 2 <= 0xFFFFFFFFull;
+    if (cfg >= 11 && cfg <= 16 && !dma_ok) cfg = 4;
+    if (cfg == 17 && (K % 64) != 0) cfg = 4;
     const bool k64 = (K % 128) == 0;
-    const int bm =
-        (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8 || cfg == 9) ? 256 : (cfg == 3 ? 64 : 128);
-    const int bn = (cfg == 4 || cfg == 5 || cfg == 6 || cfg == 9) ? 256 : 128;
+    const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8 || cfg == 9 ||
+                    (cfg >= 11 && cfg <= 13) || cfg >= 15)
+                       ? 256
+                       : (cfg == 3 ? 64 : 128);
+    const int bn = (cfg == 4 || cfg == 5 || cfg == 6 || cfg == 9 || (cfg >= 11 && cfg <= 13) || cfg >= 15) ? 256 : 128;
     const int tm = (M + bm - 1) / bm, tn = (N + bn - 1) / bn;
     const int nb = tm * tn;
 #define ALR_GEMM(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                      \
@@ -340,7 +348,23 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
 #define ALR_GEMM_WD(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                   \
   gemm_bf16_wd_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                       \
       <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, M, N, K, tm, tn, epi)
+#define ALR_GEMM_DMA(BM_, BN_, WGM_, WGN_, NS_, OCC_)                                  \
+  gemm_bf16_dma_kernel<TAG, BM_, BN_, WGM_, WGN_, NS_, OCC_, Epi>                      \
+      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
     switch (cfg) {
+      case 11: ALR_GEMM_DMA(256, 256, 2, 4, 4, 1); break;
+      case 12: ALR_GEMM_DMA(256, 256, 2, 4, 5, 1); break;
+      case 13: ALR_GEMM_DMA(256, 256, 2, 2, 4, 1); break;
+      case 14: ALR_GEMM_DMA(128, 128, 2, 2, 4, 2); break;
+      case 15:
+        gemm_bf16_pp_kernel<TAG, 4, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+        break;
+      case 16:
+        gemm_bf16_pp_kernel<TAG, 5, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+        break;
+      case 17:
+        gemm_bf16_pp64_kernel<TAG, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+        break;
       case 9: ALR_GEMM_R3(256, 256, 2, 4, 1); break;
       case 10: ALR_GEMM_R3(128, 128, 2, 2, 2); break;
       case 6: ALR_GEMM_WD(256, 256, 2, 4, 32, 1); break;
@@ -355,6 +379,7 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
 #undef ALR_GEMM
 #undef ALR_GEMM_R3
 #undef ALR_GEMM_WD
+#undef ALR_GEMM_DMA
   } else {
     const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
     gemm_f32_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
@@ -979,7 +1004,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || tile > 10) return ALR_E_INVALID_ARG;
+  if (tile < 0 || tile > 17) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
