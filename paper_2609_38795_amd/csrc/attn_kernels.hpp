@@ -118,7 +118,12 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 // in flight while the current one is consumed.
 
 constexpr int AT_KT = 64;
-constexpr int AT_DECODE_CHUNK = 512;  // keys per decode work item
+// Decode split: the shared keys of every (anchor group, kv head) are cut into
+// chunks of a common number of 64-key tiles, chosen so that a rollout step has
+// about AT_DECODE_ITEMS work items (two per workgroup slot of a 256-CU part at
+// two workgroups per CU), but never fewer than AT_DECODE_MIN_TILES tiles each.
+constexpr int AT_DECODE_ITEMS = 1024;
+constexpr int AT_DECODE_MIN_TILES = 4;
 
 template <int NCH>
 __device__ __forceinline__ int chunk_swz(int r, int c) {
@@ -142,8 +147,9 @@ struct AttnStage {
 
 // Global loads of one tile: keys k0..k0+63 of a sequence whose key 0 is token
 // row krow0 of the K cache and column vcol0 of the V^T cache.  Keys beyond
-// max_key read a clamped K row and zeros for V (they are masked anyway; the
-// zeros keep unwritten padding out of the sums).
+// max_key read a clamped K row (they are masked anyway); their V entries are
+// zeroed when the tile is written to LDS (attn_lstore), which keeps unwritten
+// padding out of the sums without waiting for the loads here.
 template <int HD>
 __device__ __forceinline__ void attn_gload(AttnStage<HD>& st, const bf16* __restrict__ Kc,
                                            long kv_rs, int kvh, long krow0,
@@ -159,24 +165,14 @@ __device__ __forceinline__ void attn_gload(AttnStage<HD>& st, const bf16* __rest
 #pragma unroll
   for (int i = 0; i < HD / 32; ++i) {
     const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
-    const int kf = k0 + c * 8;
-    u32x4 v = *(const u32x4*)(vT + (long)(kvh * HD + dim) * vt_stride + vcol0 + kf);
-    if (kf + 7 > max_key) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int ka = kf + 2 * e;
-        uint32_t w = v[e];
-        if (ka > max_key) w &= 0xFFFF0000u;
-        if (ka + 1 > max_key) w &= 0x0000FFFFu;
-        v[e] = w;
-      }
-    }
-    st.v[i] = v;
+    st.v[i] = *(const u32x4*)(vT + (long)(kvh * HD + dim) * vt_stride + vcol0 + k0 + c * 8);
   }
 }
 
+// LDS store of one tile; V entries of keys k0 + j > max_key are zeroed.
 template <int HD>
-__device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD>& t) {
+__device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD>& t, int k0,
+                                            int max_key) {
   constexpr int NCHK = HD / 8;
   const int tid = threadIdx.x;
 #pragma unroll
@@ -188,12 +184,24 @@ __device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD
   for (int i = 0; i < HD / 32; ++i) {
     const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
     const int g = c >> 1, q = c & 1;  // 16-key group, which half of it
+    u32x4 v = st.v[i];
+    const int kf = k0 + c * 8;
+    if (kf + 7 > max_key) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int ka = kf + 2 * e;
+        uint32_t w = v[e];
+        if (ka > max_key) w &= 0xFFFF0000u;
+        if (ka + 1 > max_key) w &= 0x0000FFFFu;
+        v[e] = w;
+      }
+    }
     // keys 8c..8c+3 -> chunk 2g (half q); keys 8c+4..8c+7 -> chunk 2g+1 (half q)
     u32x2 lo, hi;
-    lo[0] = st.v[i][0];
-    lo[1] = st.v[i][1];
-    hi[0] = st.v[i][2];
-    hi[1] = st.v[i][3];
+    lo[0] = v[0];
+    lo[1] = v[1];
+    hi[0] = v[2];
+    hi[1] = v[3];
     *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g) * 8 + q * 4) = lo;
     *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g + 1) * 8 + q * 4) = hi;
   }
@@ -335,7 +343,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
   const int nt = wg_last_q / AT_KT + 1;
   AttnStage<HD> st;
   attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, 0, w.len - 1);
-  attn_lstore<HD>(st, tiles[0]);
+  attn_lstore<HD>(st, tiles[0], 0, w.len - 1);
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = it * AT_KT;
@@ -347,7 +355,7 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
       else
         attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
     }
-    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
+    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1], k0 + AT_KT, w.len - 1);
     __syncthreads();
   }
   if (active && q_pos < w.len)
@@ -357,21 +365,22 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
 // Decode work item: a group of up to 128/rep consecutive sorted anchors of one
 // sequence, one kv head, and the shared keys [kbeg, kend) of that sequence.
 // The item writes, per row (anchor-major, then head within the group), the
-// partial softmax state: running max m and sum l (log2 domain) and the
-// unnormalised output; attn_decode_combine_kernel merges the items of a group
-// (the item holding the final chunk also folds in the anchor's private keys).
+// partial softmax state over those keys: running max m and sum l (log2
+// domain) and the unnormalised output.  attn_decode_combine_kernel merges the
+// items of a group and adds the anchors' private rollout keys.  An item with
+// count = 0 is padding and does nothing.
 struct DecodeItem {
-  int first, count, kvh, krow0, vcol0, kbeg, kend, part, last;  // last: final chunk of the group
+  int first, count, kvh, krow0, vcol0, kbeg, kend, part;
 };
 
 template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ vT,
-    long vt_stride, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp, long priv_rs,
-    int n_priv, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
+    long vt_stride, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
     float* __restrict__ part_o, float* __restrict__ part_ml, AttnGeom g) {
   __shared__ AttnTile<HD> tiles[2];
   const DecodeItem w = work[blockIdx.x];
+  if (w.count == 0) return;  // uniform over the workgroup
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, h = lane >> 5, lr = lane & 31;
   const int rep = g.H / g.G;
   const int rho = wave * 32 + lr;  // row within the group: anchor-major
@@ -402,7 +411,7 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
   const int nt = (w.kend - w.kbeg + AT_KT - 1) / AT_KT;
   AttnStage<HD> st;
   attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg, w.kend - 1);
-  attn_lstore<HD>(st, tiles[0]);
+  attn_lstore<HD>(st, tiles[0], w.kbeg, w.kend - 1);
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = w.kbeg + it * AT_KT;
@@ -415,66 +424,10 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
       else
         attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
     }
-    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1]);
+    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1], k0 + AT_KT, w.kend - 1);
     __syncthreads();
   }
   if (!active) return;
-  if (w.last) {
-    // the anchor's private keys of slots 1..n_priv join the last chunk's softmax;
-    // lane half h holds q dims {8h + 16 ks + e}, the partner lane the rest
-    const bf16* kp = Kp + (long)arow * priv_rs + (long)w.kvh * HD;
-    const bf16* vp = Vp + (long)arow * priv_rs + (long)w.kvh * HD;
-    for (int c0 = 0; c0 < n_priv; c0 += 16) {
-      const int cn = min(16, n_priv - c0);
-      float sc[16];
-      float pmax = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        sc[j] = -INFINITY;
-        if (j < cn) {
-          float dot = 0.f;
-#pragma unroll
-          for (int ks = 0; ks < HD / 16; ++ks) {
-            const u32x4 kw = *(const u32x4*)(kp + (long)(c0 + j) * kv_rs + ks * 16 + h * 8);
-            const u32x4 qw = __builtin_bit_cast(u32x4, qbv[ks]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              dot = fmaf(bf2f((bf16)(qw[e] & 0xFFFFu)), bf2f((bf16)(kw[e] & 0xFFFFu)), dot);
-              dot = fmaf(bf2f((bf16)(qw[e] >> 16)), bf2f((bf16)(kw[e] >> 16)), dot);
-            }
-          }
-          dot += __shfl_xor(dot, 32);
-          sc[j] = dot;  // raw score, like m
-          pmax = fmaxf(pmax, sc[j]);
-        }
-      }
-      const float m_new = fmaxf(m, pmax);
-      const float mref = m_new * g.scale_log2;
-      const float alpha = fast_exp2(m * g.scale_log2 - mref);
-#pragma unroll
-      for (int db = 0; db < HD / 32; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      float psum = 0.f;
-      for (int j = 0; j < cn; ++j) {
-        const float p = fast_exp2(fmaf(sc[j], g.scale_log2, -mref));
-        psum += p;
-        const bf16* vj = vp + (long)(c0 + j) * kv_rs;
-#pragma unroll
-        for (int db = 0; db < HD / 32; ++db)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const u32x2 vv = *(const u32x2*)(vj + db * 32 + 8 * i + 4 * h);
-            o[db][4 * i] = fmaf(p, bf2f((bf16)(vv[0] & 0xFFFFu)), o[db][4 * i]);
-            o[db][4 * i + 1] = fmaf(p, bf2f((bf16)(vv[0] >> 16)), o[db][4 * i + 1]);
-            o[db][4 * i + 2] = fmaf(p, bf2f((bf16)(vv[1] & 0xFFFFu)), o[db][4 * i + 2]);
-            o[db][4 * i + 3] = fmaf(p, bf2f((bf16)(vv[1] >> 16)), o[db][4 * i + 3]);
-          }
-      }
-      l = l * alpha + psum;
-      m = m_new;
-    }
-  }
   const long prow = (long)w.part * 128 + rho;
   float* po = part_o + prow * HD;
 #pragma unroll
@@ -499,47 +452,124 @@ struct DecodeGroup {
   int first, nchunk, part0;  // part index of (kv head 0, chunk 0); kv head g adds g*nchunk
 };
 
-// One wave per (sorted anchor r, query head j): merge the chunk partials of
-// its group (log2-domain max m, sum l, unnormalised output) into the
-// attention output.  Lanes own dims lane + 64 e; the loads of different
-// chunks are independent, so they are issued together.
+// One wave per (sorted anchor r, kv head): for each query head j of the kv
+// head's group it merges the chunk partials of the shared keys (log2-domain
+// max m, sum l, unnormalised output) and then the anchor's private rollout
+// keys 1..n_priv (one softmax over both), and writes the attention output.
+// A head is handled by HD/8 lanes with 8 dimensions each, so one pass covers
+// 64/(HD/8) heads and a score is a reduction over those lanes.  The private
+// key and value rows of the kv head are read by every head of the pass.
 template <int HD>
 __global__ __launch_bounds__(256) void attn_decode_combine_kernel(
     const int* __restrict__ grp_of_row, const DecodeGroup* __restrict__ groups,
-    const float* __restrict__ part_o, const float* __restrict__ part_ml, bf16* __restrict__ O,
-    int n_rows, AttnGeom g) {
+    const float* __restrict__ part_o, const float* __restrict__ part_ml,
+    const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
+    long priv_rs, int n_priv, bf16* __restrict__ O, int n_rows, AttnGeom g) {
+  constexpr int LPH = HD / 8;    // lanes per head
+  constexpr int HPP = 64 / LPH;  // heads per pass
+  constexpr int PB = 16;         // private keys per block
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const long item = (long)blockIdx.x * 4 + wave;
-  if (item >= (long)n_rows * g.H) return;  // no barrier in this kernel
-  const int r = (int)(item / g.H), j = (int)(item % g.H);
-  const int rep = g.H / g.G, kvh = j / rep;
+  if (item >= (long)n_rows * g.G) return;  // no barrier in this kernel
+  const int r = (int)(item / g.G), kvh = (int)(item % g.G);
+  const int rep = g.H / g.G;
   const DecodeGroup grp = groups[grp_of_row[r]];
-  const int rho = (r - grp.first) * rep + j % rep;
-  constexpr int DPL = HD / 64;  // dims per lane
-  const long p0 = (long)(grp.part0 + kvh * grp.nchunk) * 128 + rho;  // chunk c adds c*128
-  // chunk maxima: lane c reads chunk c's m (nchunk <= 64 per pass)
-  float mtot = -INFINITY;
-  for (int c0 = 0; c0 < grp.nchunk; c0 += 64) {
-    const int c = c0 + lane;
-    const float mc = (c < grp.nchunk) ? part_ml[(p0 + (long)c * 128) * 2] : -INFINITY;
-    mtot = fmaxf(mtot, wave_max(mc));
-  }
-  float ltot = 0.f, acc[DPL];
+  const int hh = lane / LPH, dl = lane % LPH;
+  const long kv_rs = (long)g.G * HD;
+  const bf16* kp = Kp + (long)r * priv_rs + (long)kvh * HD + dl * 8;
+  const bf16* vp = Vp + (long)r * priv_rs + (long)kvh * HD + dl * 8;
+  for (int j0 = 0; j0 < rep; j0 += HPP) {
+    const int jl = j0 + hh;
+    const bool act = jl < rep;
+    const int jc = act ? jl : 0;
+    const int head = kvh * rep + jc;
+    float q[8];
+    {
+      const u32x4 qw = *(const u32x4*)(Q + ((long)r * g.H + head) * HD + dl * 8);
 #pragma unroll
-  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+      for (int e = 0; e < 4; ++e) {
+        q[2 * e] = bf2f((bf16)(qw[e] & 0xFFFFu));
+        q[2 * e + 1] = bf2f((bf16)(qw[e] >> 16));
+      }
+    }
+    // shared keys: merge the chunk partials
+    const int rho = (r - grp.first) * rep + jc;
+    const long p0 = (long)(grp.part0 + kvh * grp.nchunk) * 128 + rho;  // chunk c adds c*128
+    // chunk maxima: the LPH lanes of a head read LPH chunks at a time
+    float mt = -INFINITY;
+    for (int c0 = 0; c0 < grp.nchunk; c0 += LPH) {
+      const int c = c0 + dl;
+      mt = fmaxf(mt, c < grp.nchunk ? part_ml[(p0 + (long)c * 128) * 2] : -INFINITY);
+    }
+#pragma unroll
+    for (int off = LPH / 2; off > 0; off >>= 1) mt = fmaxf(mt, __shfl_xor(mt, off));
+    float lt = 0.f, acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
 #pragma unroll 4
-  for (int c = 0; c < grp.nchunk; ++c) {
-    const long prow = p0 + (long)c * 128;
-    const float mc = part_ml[prow * 2];
-    const float a = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mtot);
-    ltot = fmaf(part_ml[prow * 2 + 1], a, ltot);
+    for (int c = 0; c < grp.nchunk; ++c) {
+      const long prow = p0 + (long)c * 128;
+      const float mc = part_ml[prow * 2];
+      const float a = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mt);
+      lt = fmaf(part_ml[prow * 2 + 1], a, lt);
+      const f32x4 o0 = *(const f32x4*)(part_o + prow * HD + dl * 8);
+      const f32x4 o1 = *(const f32x4*)(part_o + prow * HD + dl * 8 + 4);
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = fmaf(part_o[prow * HD + lane + 64 * e], a, acc[e]);
+      for (int e = 0; e < 4; ++e) {
+        acc[e] = fmaf(o0[e], a, acc[e]);
+        acc[4 + e] = fmaf(o1[e], a, acc[4 + e]);
+      }
+    }
+    // private keys, in blocks of PB: all key and value rows of a block are
+    // loaded first (rows past n_priv re-read the last valid one), then the
+    // scores, one rescale, and the weighted values
+    for (int t0 = 0; t0 < n_priv; t0 += PB) {
+      const int tn = min(PB, n_priv - t0);
+      u32x4 kw[PB], vw[PB];
+#pragma unroll
+      for (int t = 0; t < PB; ++t) kw[t] = *(const u32x4*)(kp + (long)(t0 + min(t, tn - 1)) * kv_rs);
+#pragma unroll
+      for (int t = 0; t < PB; ++t) vw[t] = *(const u32x4*)(vp + (long)(t0 + min(t, tn - 1)) * kv_rs);
+      float sc[PB];
+      float bmax = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < PB; ++t) {
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dot = fmaf(q[2 * e], bf2f((bf16)(kw[t][e] & 0xFFFFu)), dot);
+          dot = fmaf(q[2 * e + 1], bf2f((bf16)(kw[t][e] >> 16)), dot);
+        }
+#pragma unroll
+        for (int off = LPH / 2; off > 0; off >>= 1) dot += __shfl_xor(dot, off);
+        sc[t] = (t < tn) ? dot * g.scale_log2 : -INFINITY;
+        bmax = fmaxf(bmax, sc[t]);
+      }
+      const float mn = fmaxf(mt, bmax);
+      const float alpha = (mt == -INFINITY) ? 0.f : fast_exp2(mt - mn);
+      lt *= alpha;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] *= alpha;
+#pragma unroll
+      for (int t = 0; t < PB; ++t) {
+        const float p = (t < tn) ? fast_exp2(sc[t] - mn) : 0.f;
+        lt += p;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] = fmaf(p, bf2f((bf16)(vw[t][e] & 0xFFFFu)), acc[2 * e]);
+          acc[2 * e + 1] = fmaf(p, bf2f((bf16)(vw[t][e] >> 16)), acc[2 * e + 1]);
+        }
+      }
+      mt = mn;
+    }
+    if (act) {
+      const float inv = 1.f / lt;
+      u32x4 ow;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ow[e] = pack2bf(acc[2 * e] * inv, acc[2 * e + 1] * inv);
+      *(u32x4*)(O + ((long)r * g.H + head) * HD + dl * 8) = ow;
+    }
   }
-  const float inv = 1.f / ltot;
-  bf16* out = O + (long)r * g.H * HD + (long)j * HD;
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) out[lane + 64 * e] = f2bf(acc[e] * inv);
 }
 
 }  // namespace alr

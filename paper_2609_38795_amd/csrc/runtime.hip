@@ -178,8 +178,9 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
   const size_t ag = (size_t)anchor_group(c);
   L.max_groups = (NA + ag - 1) / ag + std::min<size_t>(lim.max_seqs, NA);
-  const size_t max_chunks = ((size_t)c.max_pos + AT_DECODE_CHUNK - 1) / AT_DECODE_CHUNK;
-  L.max_dwork = mfma_attn(c) ? L.max_groups * G * max_chunks : 0;
+  // chunks of >= ceil(total tiles / AT_DECODE_ITEMS) tiles: at most AT_DECODE_ITEMS full
+  // chunks plus one partial chunk per (group, kv head), plus padding to a multiple of 8
+  L.max_dwork = mfma_attn(c) ? AT_DECODE_ITEMS + L.max_groups * G + 8 : 0;
   L.i_pwork = take(L.max_pwork * sizeof(PrefillItem));
   L.i_dwork = take(L.max_dwork * sizeof(DecodeItem));
   L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
@@ -491,22 +492,22 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
       const DecodeItem* wk = ctx->at<DecodeItem>(L.i_dwork);
       float* po = ctx->at<float>(L.part_o);
       float* pml = ctx->at<float>(L.part_ml);
-      const unsigned ncomb = (unsigned)(((long)M * H + 3) / 4);
+      const unsigned ncomb = (unsigned)(((long)M * G + 3) / 4);
       const int* grow = ctx->at<int>(L.i_grprow);
       const DecodeGroup* grp = ctx->at<DecodeGroup>(L.i_groups);
       if constexpr (std::is_same<T, bf16>::value) {
         if (hd == 128) {
-          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, kp, vp,
-                                                            priv_rs, s, ctx->at<int>(L.i_apos), wk,
-                                                            po, pml, g);
+          attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride,
+                                                            ctx->at<int>(L.i_apos), wk, po, pml, g);
           ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
-          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, at, M, g);
+          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, qb, kp, vp,
+                                                                 priv_rs, s, at, M, g);
         } else {
-          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride, kp, vp,
-                                                           priv_rs, s, ctx->at<int>(L.i_apos), wk,
-                                                           po, pml, g);
+          attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride,
+                                                           ctx->at<int>(L.i_apos), wk, po, pml, g);
           ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
-          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, at, M, g);
+          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, qb, kp, vp,
+                                                                priv_rs, s, at, M, g);
         }
       }
     } else {
@@ -940,9 +941,18 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
   ctx->h_groups.clear();
   ctx->h_grprow.assign(n, 0);
   if (mfma_attn(c)) {
-    // groups of up to 128/rep sorted anchors of one sequence; each group x kv
-    // head x 512-key chunk of its shared prefix is one work item
-    const int ag = anchor_group(c);
+    // Groups of up to 128/rep sorted anchors of one sequence.  The shared keys
+    // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
+    // at absolute key positions, so the groups of one sequence read the same
+    // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
+    // dealt so that consecutive items run on one XCD (workgroup b is
+    // dispatched to XCD b % 8): the groups sharing a chunk meet in that L2.
+    const int ag = anchor_group(c), G = c.n_kv_heads;
+    struct Grp {
+      int f, cnt, sq, a_max, ntile;
+    };
+    std::vector<Grp> gs;
+    long total_tiles = 0;
     for (int r0 = 0; r0 < n;) {
       const int sq = anchor_seq[order[r0]];
       int r1 = r0;
@@ -950,20 +960,46 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
       for (int f = r0; f < r1; f += ag) {
         const int cnt = std::min(ag, r1 - f);
         const int a_max = apos[f + cnt - 1];
-        const int nchunk = (a_max + AT_DECODE_CHUNK) / AT_DECODE_CHUNK;
-        const int gi = (int)ctx->h_groups.size();
-        const int part0 = (int)ctx->h_dwork.size();
-        ctx->h_groups.push_back(DecodeGroup{f, nchunk, part0});
-        for (int rr = f; rr < f + cnt; ++rr) ctx->h_grprow[rr] = gi;
-        for (int g = 0; g < c.n_kv_heads; ++g)
-          for (int ch = 0; ch < nchunk; ++ch) {
-            const int kb = ch * AT_DECODE_CHUNK;
-            const int ke = std::min(a_max + 1, kb + AT_DECODE_CHUNK);
-            ctx->h_dwork.push_back(DecodeItem{f, cnt, g, ctx->seq_off[sq], ctx->seq_vcol[sq], kb,
-                                              ke, (int)ctx->h_dwork.size(), ch == nchunk - 1});
-          }
+        gs.push_back(Grp{f, cnt, sq, a_max, (a_max + AT_KT) / AT_KT});
+        total_tiles += (long)gs.back().ntile * G;
       }
       r0 = r1;
+    }
+    const int ct = (int)std::max<long>(AT_DECODE_MIN_TILES,
+                                       (total_tiles + AT_DECODE_ITEMS - 1) / AT_DECODE_ITEMS);
+    int part = 0;
+    for (size_t gi = 0; gi < gs.size(); ++gi) {
+      const int nchunk = (gs[gi].ntile + ct - 1) / ct;
+      ctx->h_groups.push_back(DecodeGroup{gs[gi].f, nchunk, part});
+      for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) ctx->h_grprow[rr] = (int)gi;
+      part += nchunk * G;
+    }
+    std::vector<DecodeItem> logical;
+    for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
+      size_t g1 = g0;
+      int max_chunks = 0;
+      while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
+        max_chunks = std::max(max_chunks, ctx->h_groups[g1].nchunk);
+        ++g1;
+      }
+      const int sq = gs[g0].sq;
+      for (int g = 0; g < G; ++g)
+        for (int ch = 0; ch < max_chunks; ++ch)
+          for (size_t gi = g0; gi < g1; ++gi) {
+            const DecodeGroup& dg = ctx->h_groups[gi];
+            if (ch >= dg.nchunk) continue;
+            const int kb = ch * ct * AT_KT;
+            const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
+            logical.push_back(DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[sq],
+                                         ctx->seq_vcol[sq], kb, ke, dg.part0 + g * dg.nchunk + ch});
+          }
+      g0 = g1;
+    }
+    const size_t per = (logical.size() + 7) / 8;
+    ctx->h_dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
+    for (size_t b = 0; b < per * 8; ++b) {
+      const size_t li = (b % 8) * per + b / 8;
+      if (li < logical.size()) ctx->h_dwork[b] = logical[li];
     }
   }
   if (ctx->h_dwork.size() > ctx->L.max_dwork || ctx->h_groups.size() > ctx->L.max_groups)
