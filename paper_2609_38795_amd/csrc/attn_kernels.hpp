@@ -119,10 +119,12 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 
 constexpr int AT_KT = 64;
 // Decode split: the shared keys of every (anchor group, kv head) are cut into
-// chunks of a common number of 64-key tiles, chosen so that a rollout step has
-// about AT_DECODE_ITEMS work items (two per workgroup slot of a 256-CU part at
-// two workgroups per CU), but never fewer than AT_DECODE_MIN_TILES tiles each.
-constexpr int AT_DECODE_ITEMS = 1024;
+// chunks of a common number ct of 64-key tiles.  The host picks ct to
+// minimise (rounds of workgroups) x (ct + AT_DECODE_ITEM_OVERHEAD), with two
+// workgroups per CU, among the ct that give at most AT_DECODE_MAX_ITEMS items
+// and never fewer than AT_DECODE_MIN_TILES tiles per item.
+constexpr int AT_DECODE_MAX_ITEMS = 2048;
+constexpr int AT_DECODE_ITEM_OVERHEAD = 3;  // prologue, partial store and merge, in tiles
 constexpr int AT_DECODE_MIN_TILES = 4;
 
 template <int NCH>
@@ -243,7 +245,7 @@ __device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf
       }
       tmax = fmaxf(tmax, s[kb][r]);
     }
-  tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+  tmax = max_xor32(tmax);
   const float m_new = fmaxf(m, tmax);
   const float mref = (m_new == -INFINITY) ? 0.f : m_new * scale_log2;
   const bool grew = m_new > m;
@@ -257,7 +259,7 @@ __device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf
       s[kb][r] = p;
       psum += p;
     }
-  psum += __shfl_xor(psum, 32);
+  psum = sum_xor32(psum);
   l = l * alpha + psum;
   m = m_new;
   if (__any(grew)) {

@@ -54,6 +54,18 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// max / sum of v over lanes i and i ^ 32: v_permlane32_swap exchanges the two
+// 32-lane halves of the wave in registers (no LDS round trip); the pair it
+// returns holds both halves' values in every lane.  All lanes must be active.
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // 2^x on the hardware exp unit (v_exp_f32): results below 2^-126 flush to 0,
 // which softmax weights can afford; -inf gives 0.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

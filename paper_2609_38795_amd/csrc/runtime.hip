@@ -178,9 +178,9 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
   const size_t ag = (size_t)anchor_group(c);
   L.max_groups = (NA + ag - 1) / ag + std::min<size_t>(lim.max_seqs, NA);
-  // chunks of >= ceil(total tiles / AT_DECODE_ITEMS) tiles: at most AT_DECODE_ITEMS full
-  // chunks plus one partial chunk per (group, kv head), plus padding to a multiple of 8
-  L.max_dwork = mfma_attn(c) ? AT_DECODE_ITEMS + L.max_groups * G + 8 : 0;
+  // chunks of >= ceil(total tiles / AT_DECODE_MAX_ITEMS) tiles: at most AT_DECODE_MAX_ITEMS
+  // full chunks plus one partial chunk per (group, kv head), plus padding to a multiple of 8
+  L.max_dwork = mfma_attn(c) ? AT_DECODE_MAX_ITEMS + L.max_groups * G + 8 : 0;
   L.i_pwork = take(L.max_pwork * sizeof(PrefillItem));
   L.i_dwork = take(L.max_dwork * sizeof(DecodeItem));
   L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
@@ -251,6 +251,7 @@ struct alr_ctx {
   size_t ws_bytes;
   Layout L;
   bool prefilled = false;
+  int n_cu = 256;  // compute units of the device (sizes the decode work split)
   int n_seq = 0;
   std::vector<int> seq_len, seq_off;
   std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
@@ -740,6 +741,12 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
     }                                                                                \
   } while (0)
 
+  {
+    int dev = 0, ncu = 0;
+    CREATE_HIP(hipGetDevice(&dev));
+    CREATE_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
+    ctx->n_cu = std::max(1, ncu);
+  }
   const size_t es = L.es, d = c.d_model, F = c.d_ffn, V = c.vocab;
   const int H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
   const size_t qd = (size_t)H * hd, kvd = (size_t)G * hd;
@@ -965,8 +972,22 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
       }
       r0 = r1;
     }
-    const int ct = (int)std::max<long>(AT_DECODE_MIN_TILES,
-                                       (total_tiles + AT_DECODE_ITEMS - 1) / AT_DECODE_ITEMS);
+    int max_nt = 1;
+    for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
+    const int ct_min = (int)std::max<long>(
+        AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
+    const long slots = 2L * ctx->n_cu;
+    int ct = std::max(ct_min, max_nt);
+    double best = -1.0;
+    for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
+      long items = 0;
+      for (const Grp& gr : gs) items += (long)((gr.ntile + cand - 1) / cand) * G;
+      const double cost = (double)((items + slots - 1) / slots) * (cand + AT_DECODE_ITEM_OVERHEAD);
+      if (best < 0 || cost < best) {
+        best = cost;
+        ct = cand;
+      }
+    }
     int part = 0;
     for (size_t gi = 0; gi < gs.size(); ++gi) {
       const int nchunk = (gs[gi].ntile + ct - 1) / ct;
