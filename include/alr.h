@@ -172,6 +172,88 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
                        int32_t* tokens_out, float* logprobs_out, float* feats_out,
                        alr_stream stream);
 
+/* Number of most probable tokens a label keeps (the paper's distillation
+ * loss: top 8 probabilities plus one bucket for the remaining mass). */
+#define ALR_TOPK 8
+
+/* Greedy rollout with labels in the paper's loss format (Sec. 3.1, Eq. 1; App.
+ * A, the loss row of the training table and "Rollout implementation": the 8
+ * most probable tokens of each slot plus the remaining mass).  Arguments as in
+ * alr_rollout, plus:
+ *   top_ids_out  DEVICE int32 [n_anchor, block, ALR_TOPK]: token ids ranked by
+ *                decreasing probability, equal probabilities by increasing id
+ *                (entry 0 is the greedy token).
+ *   top_logp_out DEVICE fp32 [n_anchor, block, ALR_TOPK]: their log-probs.
+ *   tail_out     DEVICE fp32 [n_anchor, block]: probability summed over every
+ *                other token (summed directly, not as 1 - top mass).
+ *   logprobs_out DEVICE fp32 [n_anchor, block, vocab] or NULL: the full
+ *                log-softmax as in alr_rollout.  When NULL the logits of each
+ *                step go to workspace rows and only the compact labels (4 +
+ *                68 bytes per slot) reach the caller.
+ * Tokens, features and the top-8 labels are identical whether or not the full
+ * log-probs are requested.  Same checks and status codes as alr_rollout. */
+alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                            const int32_t* anchor_pos, int32_t block, const int32_t* forced,
+                            int32_t* tokens_out, int32_t* top_ids_out, float* top_logp_out,
+                            float* tail_out, float* logprobs_out, float* feats_out,
+                            alr_stream stream);
+
+/* Fixed-corpus distillation labels and erase gates (Sec. 3.1: the KD labels
+ * pi_{a,k} = p_T(. | x_{<a+k}), and Eq. 2, the survival gate with its hard
+ * variant), read from the last prefill's final normalised rows through the
+ * output head.  Index s = 0 .. block-1 of anchor a is the paper's slot k = s+1
+ * at position a+s; it is valid while a + s <= seq_len - 1.
+ *   anchor_seq, anchor_pos  HOST int32 [n_anchor] as in alr_rollout
+ *              (anchor_pos + block - 1 < max_pos; slots past the sequence end
+ *              are reported invalid, not rejected).
+ *   argmax_out   DEVICE int32 [n_anchor, block]: greedy token of the label
+ *                (ties -> lower id), -1 for an invalid index.
+ *   top_ids_out, top_logp_out, tail_out: as in alr_rollout_topk, or all NULL;
+ *                invalid indices get ids -1, log-probs -inf, tail 0.
+ *   logprobs_out DEVICE fp32 [n_anchor, block, vocab] or NULL (rows of -inf
+ *                at invalid indices).  At least one label form must be given.
+ *   corpus_logp_out DEVICE fp32 [n_anchor, block]: log p_T(x_{a+s+1} |
+ *                x_{<=a+s}); nan when a+s+1 is past the end or holds a given
+ *                input row (alr_prefill's embeds) instead of a token.
+ *   gate_soft_out DEVICE fp32 [n_anchor, block]: g = exp(sum over earlier
+ *                indices of corpus_logp); 1 at index 0; 0 at invalid indices
+ *                and after an undefined factor.
+ *   gate_hard_out DEVICE fp32 [n_anchor, block]: product over earlier indices
+ *                of [argmax == corpus token], same conventions.
+ * Outputs are in the caller's anchor order.  Same host checks as
+ * alr_rollout. */
+alr_status alr_corpus_labels(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                             const int32_t* anchor_pos, int32_t block, int32_t* argmax_out,
+                             int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                             float* logprobs_out, float* corpus_logp_out, float* gate_soft_out,
+                             float* gate_hard_out, alr_stream stream);
+
+/* Secondary blocks of in-rollout anchors (Sec. 3.2, Eq. 4), gathered from the
+ * outputs of alr_rollout_topk over n_primary primary blocks of `block` slots
+ * (no target computation).  Secondary q sits at offset j = sec_offset[q] of
+ * primary p = sec_primary[q] (HOST arrays [n_secondary]; 0 <= p < n_primary,
+ * 1 <= j <= block-1; the paper draws j uniformly from 2 .. K-1 with K =
+ * block-1).  Inputs tokens [n_primary, block], top_ids/top_logp
+ * [n_primary, block, ALR_TOPK], tail [n_primary, block] are DEVICE arrays.
+ *   token0_out  DEVICE int32 [n_secondary]: slot-0 token y*_j = tokens[p, j-1];
+ *               the block's slot 0 sits at position anchor_pos[p] + j and its
+ *               context is the prefix up to the anchor plus the primary's
+ *               rollout positions 1 .. j-1 (their features are the primary's
+ *               feature rows 1 .. j-1).
+ *   top_ids_out, top_logp_out [n_secondary, block, ALR_TOPK], tail_out
+ *               [n_secondary, block]: index s' holds the primary's labels at
+ *               index j + s' (paper slot j + k with k = s'+1) while j + s' <=
+ *               block-1, else ids -1, log-probs -inf, tail 0.
+ *   weight_out  DEVICE fp32 [n_secondary, block]: w_k = exp(-(k-1)/gamma)
+ *               where j + k <= block-1, else 0 (unsupervised tail).
+ * gamma > 0.  n_secondary = 0 is a no-op. */
+alr_status alr_ira_assemble(alr_ctx* ctx, int32_t n_primary, int32_t block,
+                            const int32_t* tokens, const int32_t* top_ids, const float* top_logp,
+                            const float* tail, int32_t n_secondary, const int32_t* sec_primary,
+                            const int32_t* sec_offset, float gamma, int32_t* token0_out,
+                            int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                            float* weight_out, alr_stream stream);
+
 /* Message of the last failing call on ctx ("" if none); ctx may be NULL, then
  * the message of the last failing alr_create in this thread is returned. */
 const char* alr_last_error(const alr_ctx* ctx);

@@ -23,8 +23,10 @@ STATUS = {0: "ALR_OK", 1: "ALR_E_INVALID_ARG", 2: "ALR_E_OUT_OF_RANGE", 3: "ALR_
 
 # Every function the C headers declare (include/alr.h, include/alr_debug.h).
 EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_create",
-           "alr_prefill", "alr_rollout", "alr_last_error", "alr_status_string", "alr_destroy",
+           "alr_prefill", "alr_rollout", "alr_rollout_topk", "alr_corpus_labels",
+           "alr_ira_assemble", "alr_last_error", "alr_status_string", "alr_destroy",
            "alr_debug_gemm", "alr_profile_start", "alr_profile_stop")
+ALR_TOPK = 8
 
 
 class AlrConfig(ctypes.Structure):
@@ -87,6 +89,14 @@ def load_library() -> ctypes.CDLL:
     lib.alr_prefill.restype = ctypes.c_int
     lib.alr_rollout.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp]
     lib.alr_rollout.restype = ctypes.c_int
+    lib.alr_rollout_topk.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.alr_rollout_topk.restype = ctypes.c_int
+    lib.alr_corpus_labels.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                      vp]
+    lib.alr_corpus_labels.restype = ctypes.c_int
+    lib.alr_ira_assemble.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, i32p, i32p,
+                                     ctypes.c_float, vp, vp, vp, vp, vp, vp]
+    lib.alr_ira_assemble.restype = ctypes.c_int
     lib.alr_last_error.argtypes = [vp]
     lib.alr_last_error.restype = ctypes.c_char_p
     lib.alr_status_string.argtypes = [ctypes.c_int]
@@ -254,6 +264,88 @@ class Engine:
         if st != 0:
             self._err(st)
         return tok, lp, ft
+
+
+    def alloc_topk(self, n: int, block: int):
+        torch = self.torch
+        return (torch.empty((n, block, ALR_TOPK), dtype=torch.int32, device=self.device),
+                torch.empty((n, block, ALR_TOPK), dtype=torch.float32, device=self.device),
+                torch.empty((n, block), dtype=torch.float32, device=self.device))
+
+    def rollout_topk(self, anchor_seq, anchor_pos, block: int, forced=None,
+                     want_logprobs: bool = False, want_feats: bool = True, out=None):
+        """-> (tokens, top_ids, top_logp, tail, logprobs or None, feats or None)."""
+        torch = self.torch
+        a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+        a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+        n = len(a_s)
+        if out is None:
+            tok = torch.empty((n, block), dtype=torch.int32, device=self.device)
+            ti, tl, tt = self.alloc_topk(n, block)
+            lp = (torch.empty((n, block, self.shape.vocab), dtype=torch.float32,
+                              device=self.device) if want_logprobs else None)
+            ft = None
+            if want_feats and self.shape.n_feat > 0:
+                ft = torch.empty((n, block, self.shape.n_feat, self.shape.d_model),
+                                 dtype=torch.float32, device=self.device)
+        else:
+            tok, ti, tl, tt, lp, ft = out
+        st = self.lib.alr_rollout_topk(
+            self.ctx, n, _i32p(a_s), _i32p(a_p), block,
+            None if forced is None else forced.data_ptr(), tok.data_ptr(), ti.data_ptr(),
+            tl.data_ptr(), tt.data_ptr(), None if lp is None else lp.data_ptr(),
+            None if ft is None else ft.data_ptr(), self._sp())
+        if st != 0:
+            self._err(st)
+        return tok, ti, tl, tt, lp, ft
+
+    def corpus_labels(self, anchor_seq, anchor_pos, block: int, want_topk: bool = True,
+                      want_logprobs: bool = False):
+        """-> dict of argmax, top_ids, top_logp, tail, logprobs, corpus_logp, gate_soft,
+        gate_hard (device tensors; absent forms are None)."""
+        torch = self.torch
+        a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+        a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+        n = len(a_s)
+        f32 = dict(dtype=torch.float32, device=self.device)
+        r = {"argmax": torch.empty((n, block), dtype=torch.int32, device=self.device),
+             "top_ids": None, "top_logp": None, "tail": None, "logprobs": None,
+             "corpus_logp": torch.empty((n, block), **f32),
+             "gate_soft": torch.empty((n, block), **f32),
+             "gate_hard": torch.empty((n, block), **f32)}
+        if want_topk:
+            r["top_ids"], r["top_logp"], r["tail"] = self.alloc_topk(n, block)
+        if want_logprobs:
+            r["logprobs"] = torch.empty((n, block, self.shape.vocab), **f32)
+        ptr = (lambda t: None if t is None else t.data_ptr())
+        st = self.lib.alr_corpus_labels(
+            self.ctx, n, _i32p(a_s), _i32p(a_p), block, ptr(r["argmax"]), ptr(r["top_ids"]),
+            ptr(r["top_logp"]), ptr(r["tail"]), ptr(r["logprobs"]), ptr(r["corpus_logp"]),
+            ptr(r["gate_soft"]), ptr(r["gate_hard"]), self._sp())
+        if st != 0:
+            self._err(st)
+        return r
+
+    def ira_assemble(self, tokens, top_ids, top_logp, tail, sec_primary, sec_offset,
+                     gamma: float = 2.0):
+        """Secondary blocks from primary rollout labels -> (token0, top_ids, top_logp, tail,
+        weight) device tensors."""
+        torch = self.torch
+        n_prim, block = tokens.shape
+        sp = np.ascontiguousarray(sec_primary, dtype=np.int32)
+        so = np.ascontiguousarray(sec_offset, dtype=np.int32)
+        q = len(sp)
+        t0 = torch.empty(q, dtype=torch.int32, device=self.device)
+        ti, tl, tt = self.alloc_topk(q, block)
+        w = torch.empty((q, block), dtype=torch.float32, device=self.device)
+        st = self.lib.alr_ira_assemble(self.ctx, n_prim, block, tokens.data_ptr(),
+                                       top_ids.data_ptr(), top_logp.data_ptr(), tail.data_ptr(),
+                                       q, _i32p(sp), _i32p(so), gamma, t0.data_ptr(),
+                                       ti.data_ptr(), tl.data_ptr(), tt.data_ptr(), w.data_ptr(),
+                                       self._sp())
+        if st != 0:
+            self._err(st)
+        return t0, ti, tl, tt, w
 
 
 PROF_SITES = {"prefill_qkv": 1, "prefill_attn": 2, "prefill_o": 3, "prefill_gu": 4,

@@ -90,12 +90,39 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(char* __restrict__ ds
   for (long c = threadIdx.x; c < row_bytes / 16; c += blockDim.x) o[c] = s[c];
 }
 
-// Output head finalisation for the sorted row r of rollout slot s.
-//   row data: logits (fp32) at lp + perm[r] * row_stride, V entries, written by
-//   the output-head GEMM.  Computes max, argmax (ties -> lowest id) and
-//   sum(exp(z - max)) in one pass, then overwrites the row with z - LSE.
-//   tokens_out[perm[r] * block + s] = argmax; the next input token of row r is
-//   forced[perm[r] * block + s] if that is >= 0, else the argmax.
+// Output head finalisation of the sorted row r of slot s.
+//   Logits (fp32, V entries) of row r are at z + (z_perm ? perm[r] : r) * z_rs,
+//   written by the output-head GEMM.  Outputs go to index o = perm[r] * block + s
+//   (the caller's anchor order).  Pass 1 computes the max, the argmax (ties ->
+//   lowest id) and sum(exp(z - max)); with TOPK it also keeps each thread's 8
+//   best (value, id) pairs, ranked by decreasing value and then increasing id,
+//   and merges them into the row's top 8 with eight block-wide argmax rounds.
+//   Pass 2 (when write_lp or TOPK) rewrites the row as z - LSE and, with TOPK,
+//   sums exp(z - max) over the tokens ranked after the 8th (the tail bucket).
+//   next_tok[r] = forced[o] if that is >= 0, else the argmax.  target_logp[o]
+//   = log p(target[r]) (nan when target[r] < 0).  A row with valid[r] == 0 gets
+//   token -1, top ids -1, top log-probs -inf, tail 0, target log-prob nan and,
+//   when write_lp, a row of -inf.
+constexpr int ALR_K_TOP = 8;
+
+struct LmFinalize {
+  float* z;
+  long z_rs;
+  int z_perm;
+  int write_lp;
+  const int* perm;
+  int V, block, s;
+  int* tokens;         // [o] or null
+  const int* forced;   // [o] or null
+  int* next_tok;       // [r] or null
+  int* top_ids;        // [o * 8] (TOPK)
+  float* top_logp;     // [o * 8] (TOPK)
+  float* tail;         // [o] (TOPK)
+  const int* target;   // [r] or null
+  float* target_logp;  // [o] (with target)
+  const unsigned char* valid;  // [r] or null
+};
+
 struct MaxArg {
   float m, s;
   int i;
@@ -109,17 +136,47 @@ __device__ __forceinline__ MaxArg merge_maxarg(MaxArg a, MaxArg b) {
   return {a.m, a.s + sb, a.i};
 }
 
-__global__ __launch_bounds__(256) void lm_finalize_kernel(float* __restrict__ lp, long row_stride,
-                                                          const int* __restrict__ perm, int V,
-                                                          int* __restrict__ tokens_out, int block,
-                                                          int s, const int* __restrict__ forced,
-                                                          int* __restrict__ next_tok) {
+// (v, i) ranks before (w, j): larger value, then lower id
+__device__ __forceinline__ bool ranks_before(float v, int i, float w, int j) {
+  return v > w || (v == w && i < j);
+}
+
+template <bool TOPK>
+__global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   __shared__ MaxArg red[4];
-  __shared__ float lse_sh;
+  __shared__ float lse_sh, m_sh, s_sh, tgt_sh;
+  __shared__ float win_v[4], top_v[ALR_K_TOP];
+  __shared__ int win_i[4], top_i[ALR_K_TOP];
+  __shared__ float tail_red[4];
   const int r = blockIdx.x;
-  const long orow = perm[r];
-  float* z = lp + orow * row_stride;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long orow = a.perm[r];
+  const long o = orow * a.block + a.s;
+  float* z = a.z + (a.z_perm ? orow : (long)r) * a.z_rs;
+  const int V = a.V;
+  if (a.valid != nullptr && a.valid[r] == 0) {  // uniform over the block
+    if (threadIdx.x == 0) {
+      if (a.tokens) a.tokens[o] = -1;
+      if (a.next_tok) a.next_tok[r] = 0;
+      if (a.target) a.target_logp[o] = __builtin_nanf("");
+      if (TOPK) a.tail[o] = 0.f;
+    }
+    if (TOPK && threadIdx.x < ALR_K_TOP) {
+      a.top_ids[o * ALR_K_TOP + threadIdx.x] = -1;
+      a.top_logp[o * ALR_K_TOP + threadIdx.x] = -INFINITY;
+    }
+    if (a.write_lp)
+      for (int c = threadIdx.x; c < V; c += blockDim.x) z[c] = -INFINITY;
+    return;
+  }
   MaxArg acc = {-INFINITY, 0.f, 0x7FFFFFFF};
+  float tv[ALR_K_TOP];
+  int ti[ALR_K_TOP];
+#pragma unroll
+  for (int j = 0; j < ALR_K_TOP; ++j) {
+    tv[j] = -INFINITY;
+    ti[j] = 0x7FFFFFFF;
+  }
   for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
     const f32x4 v = *(const f32x4*)(z + c);
 #pragma unroll
@@ -131,39 +188,250 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(float* __restrict__ lp
       } else {
         acc.s += expf(v[e] - acc.m);
       }
+      if constexpr (TOPK) {
+        // this thread meets ids in increasing order, so an equal value ranks
+        // after the entries already held: insert only strictly larger values
+        if (v[e] > tv[ALR_K_TOP - 1]) {
+          float pv = v[e];
+          int pi = c + e;
+          bool sh = false;
+#pragma unroll
+          for (int j = 0; j < ALR_K_TOP; ++j) {
+            const bool take = sh || (v[e] > tv[j]);
+            if (take) {
+              const float ov = tv[j];
+              const int oi = ti[j];
+              tv[j] = pv;
+              ti[j] = pi;
+              pv = ov;
+              pi = oi;
+            }
+            sh = take;
+          }
+        }
+      }
     }
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
+  for (int off = 32; off > 0; off >>= 1) {
     MaxArg b;
-    b.m = __shfl_xor(acc.m, o);
-    b.s = __shfl_xor(acc.s, o);
-    b.i = __shfl_xor(acc.i, o);
+    b.m = __shfl_xor(acc.m, off);
+    b.s = __shfl_xor(acc.s, off);
+    b.i = __shfl_xor(acc.i, off);
     acc = merge_maxarg(acc, b);
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (lane == 0) red[wave] = acc;
   __syncthreads();
   if (threadIdx.x == 0) {
     MaxArg t = red[0];
     for (int w = 1; w < (int)(blockDim.x >> 6); ++w) t = merge_maxarg(t, red[w]);
     lse_sh = t.m + logf(t.s);
-    tokens_out[orow * block + s] = t.i;
-    int nxt = t.i;
-    if (forced != nullptr) {
-      const int f = forced[orow * block + s];
-      if (f >= 0) nxt = f;
+    m_sh = t.m;
+    s_sh = t.s;
+    if (a.tokens) a.tokens[o] = t.i;
+    if (a.next_tok) {
+      int nxt = t.i;
+      if (a.forced != nullptr) {
+        const int f = a.forced[o];
+        if (f >= 0) nxt = f;
+      }
+      a.next_tok[r] = nxt;
     }
-    next_tok[r] = nxt;
+    if (a.target) {
+      const int x = a.target[r];
+      tgt_sh = (x >= 0) ? z[x] : __builtin_nanf("");
+    }
   }
-  __syncthreads();
-  const float lse = lse_sh;
+  if constexpr (TOPK) {
+    // eight rounds: the best head of all threads' lists is the next entry
+    for (int k = 0; k < ALR_K_TOP; ++k) {
+      float bv = tv[0];
+      int bi = ti[0];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int oi = __shfl_xor(bi, off);
+        if (ranks_before(ov, oi, bv, bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      if (lane == 0) {
+        win_v[wave] = bv;
+        win_i[wave] = bi;
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        float wv = win_v[0];
+        int wi = win_i[0];
+        for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
+          if (ranks_before(win_v[w], win_i[w], wv, wi)) {
+            wv = win_v[w];
+            wi = win_i[w];
+          }
+        top_v[k] = wv;
+        top_i[k] = wi;
+      }
+      __syncthreads();
+      if (ti[0] == top_i[k] && tv[0] != -INFINITY) {  // ids are unique: the owner pops its head
+#pragma unroll
+        for (int j = 0; j < ALR_K_TOP - 1; ++j) {
+          tv[j] = tv[j + 1];
+          ti[j] = ti[j + 1];
+        }
+        tv[ALR_K_TOP - 1] = -INFINITY;
+        ti[ALR_K_TOP - 1] = 0x7FFFFFFF;
+      }
+    }
+  } else {
+    __syncthreads();
+  }
+  const float lse = lse_sh, m = m_sh;
+  if (!a.write_lp && !TOPK) {
+    if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
+    return;
+  }
+  const float zk = TOPK ? top_v[ALR_K_TOP - 1] : 0.f;
+  const int ik = TOPK ? top_i[ALR_K_TOP - 1] : 0;
+  float tsum = 0.f;
   for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
     f32x4 v = *(const f32x4*)(z + c);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] -= lse;
-    *(f32x4*)(z + c) = v;
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (TOPK) {
+        if (v[e] < zk || (v[e] == zk && c + e > ik)) tsum += expf(v[e] - m);
+      }
+      v[e] -= lse;
+    }
+    if (a.write_lp) *(f32x4*)(z + c) = v;
   }
+  if constexpr (TOPK) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) tsum += __shfl_xor(tsum, off);
+    if (lane == 0) tail_red[wave] = tsum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float t = 0.f;
+      for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += tail_red[w];
+      a.tail[o] = t / s_sh;
+    }
+    if (threadIdx.x < ALR_K_TOP) {
+      const bool have = top_v[threadIdx.x] != -INFINITY;
+      a.top_ids[o * ALR_K_TOP + threadIdx.x] = have ? top_i[threadIdx.x] : -1;
+      a.top_logp[o * ALR_K_TOP + threadIdx.x] = have ? top_v[threadIdx.x] - lse : -INFINITY;
+    }
+  }
+  if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
+}
+
+// Corpus-label rows of slot s: row r takes the prefill's final-norm row at
+// position min(a + s, len - 1) of its sequence (a = apos[r], len = alen[r],
+// first token row atok[r] - apos[r]); valid[r] = (a + s <= len - 1);
+// target[r] = the corpus token at a + s + 1 (from ctok, -1 for a given input
+// row) when a + s + 1 <= len - 1, else -1.
+template <typename T>
+__global__ __launch_bounds__(256) void corpus_rows_kernel(T* __restrict__ dst,
+                                                          const T* __restrict__ src,
+                                                          const int* __restrict__ atok,
+                                                          const int* __restrict__ apos,
+                                                          const int* __restrict__ alen,
+                                                          const int* __restrict__ ctok, int s,
+                                                          long row_elems,
+                                                          unsigned char* __restrict__ valid,
+                                                          int* __restrict__ target) {
+  const long r = blockIdx.x;
+  const int a = apos[r], len = alen[r], t0 = atok[r] - a;
+  const int p = min(a + s, len - 1);
+  const T* sp = src + (long)(t0 + p) * row_elems;
+  T* op = dst + r * row_elems;
+  for (long c = threadIdx.x; c < row_elems; c += blockDim.x) op[c] = sp[c];
+  if (threadIdx.x == 0) {
+    valid[r] = (a + s <= len - 1) ? 1 : 0;
+    target[r] = (a + s + 1 <= len - 1) ? ctok[t0 + a + s + 1] : -1;
+  }
+}
+
+// Erase gates of anchor row r (caller order o = perm[r]) from the per-slot
+// corpus log-probs and argmax tokens written by lm_finalize_kernel:
+// soft[s] = exp(sum_{t<s} lp[t]), hard[s] = prod_{t<s} [argmax[t] == x_{a+t+1}];
+// a slot past the sequence end gets 0 and so does everything after a factor
+// that is undefined (nan log-prob).
+__global__ __launch_bounds__(256) void erase_gates_kernel(const int* __restrict__ perm,
+                                                          const int* __restrict__ atok,
+                                                          const int* __restrict__ apos,
+                                                          const int* __restrict__ alen,
+                                                          const int* __restrict__ ctok,
+                                                          const float* __restrict__ clp,
+                                                          const int* __restrict__ amax, int n,
+                                                          int block, float* __restrict__ soft,
+                                                          float* __restrict__ hard) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= n) return;
+  const long o0 = (long)perm[r] * block;
+  const int a = apos[r], len = alen[r], t0 = atok[r] - a;
+  float cum = 0.f, h = 1.f;
+  bool alive = true;
+  for (int s = 0; s < block; ++s) {
+    if (a + s > len - 1) {
+      soft[o0 + s] = 0.f;
+      hard[o0 + s] = 0.f;
+      continue;
+    }
+    soft[o0 + s] = alive ? expf(cum) : 0.f;
+    hard[o0 + s] = alive ? h : 0.f;
+    const float lp = clp[o0 + s];
+    if (!(lp == lp)) {  // nan: no corpus token follows
+      alive = false;
+    } else {
+      cum += lp;
+      h = (amax[o0 + s] == ctok[t0 + a + s + 1]) ? h : 0.f;
+    }
+  }
+}
+
+// Secondary blocks of in-rollout anchors: secondary q sits at offset j = off[q]
+// of primary block p = prim[q] (1 <= j <= block-1).  token0[q] = tokens[p, j-1]
+// (y*_j); its index s' copies the primary's labels at index j + s' while that
+// is <= block-1 (else ids -1, log-probs -inf, tail 0); weight[q, s'] =
+// exp(-s'/gamma) when j + s' + 1 <= block - 1, else 0.  One thread per (q, s').
+__global__ __launch_bounds__(256) void ira_assemble_kernel(
+    const int* __restrict__ prim, const int* __restrict__ off, int n_sec, int block,
+    const int* __restrict__ tokens, const int* __restrict__ top_ids,
+    const float* __restrict__ top_logp, const float* __restrict__ tail, float gamma,
+    int* __restrict__ token0, int* __restrict__ s_ids, float* __restrict__ s_logp,
+    float* __restrict__ s_tail, float* __restrict__ s_weight) {
+  const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (long)n_sec * block) return;
+  const int q = (int)(t / block), s2 = (int)(t % block);
+  const int p = prim[q], j = off[q];
+  if (s2 == 0) token0[q] = tokens[(long)p * block + j - 1];
+  const long dst = (long)q * block + s2;
+  const int src = j + s2;
+  if (src <= block - 1) {
+    const long so = (long)p * block + src;
+    for (int e = 0; e < ALR_K_TOP; ++e) {
+      s_ids[dst * ALR_K_TOP + e] = top_ids[so * ALR_K_TOP + e];
+      s_logp[dst * ALR_K_TOP + e] = top_logp[so * ALR_K_TOP + e];
+    }
+    s_tail[dst] = tail[so];
+  } else {
+    for (int e = 0; e < ALR_K_TOP; ++e) {
+      s_ids[dst * ALR_K_TOP + e] = -1;
+      s_logp[dst * ALR_K_TOP + e] = -INFINITY;
+    }
+    s_tail[dst] = 0.f;
+  }
+  s_weight[dst] = (j + s2 + 1 <= block - 1) ? expf(-(float)s2 / gamma) : 0.f;
+}
+
+// Corpus tokens kept for the corpus labels: ctok[i] = tokens[i], or -1 where
+// a given input row replaces the token (mask[i] != 0).
+__global__ __launch_bounds__(256) void keep_tokens_kernel(int* __restrict__ ctok,
+                                                          const int* __restrict__ tokens,
+                                                          const unsigned char* __restrict__ mask,
+                                                          int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) ctok[i] = (mask != nullptr && mask[i]) ? -1 : tokens[i];
 }
 
 }  // namespace alr

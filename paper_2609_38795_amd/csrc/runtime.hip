@@ -31,6 +31,8 @@
 
 using namespace alr;
 
+static_assert(ALR_K_TOP == ALR_TOPK, "top-k size of the kernels and the ABI differ");
+
 namespace {
 
 thread_local std::string g_create_err;
@@ -48,7 +50,8 @@ struct Layout {
   size_t kp, vp, kvp_layer_stride;
   size_t feat_store, hf_store;
   size_t resid, xnorm, qbuf, attn, act;
-  size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_cur;
+  size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_alen, i_cur;
+  size_t i_valid, i_target, i_ira, i_ctok, logits;
   size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
   size_t max_pwork, max_dwork, max_groups;
@@ -174,7 +177,13 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_apos = take(NA * 4);
   L.i_atok = take(NA * 4);
   L.i_aseq = take(NA * 4);
+  L.i_alen = take(NA * 4);
   L.i_cur = take(NA * 4);
+  L.i_valid = take(NA);
+  L.i_target = take(NA * 4);
+  L.i_ira = take(NA * 2 * 4);
+  L.i_ctok = take(T * 4);
+  L.logits = take(NA * V * 4);
   L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
   const size_t ag = (size_t)anchor_group(c);
   L.max_groups = (NA + ag - 1) / ag + std::min<size_t>(lim.max_seqs, NA);
@@ -256,7 +265,8 @@ struct alr_ctx {
   std::vector<int> seq_len, seq_off;
   std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
   std::vector<PrefillItem> h_pwork;
-  std::vector<int> h_anch;  // perm | apos | atok | aseq, each n_anchor long
+  std::vector<int> h_anch;  // perm | apos | atok | aseq | alen, each n_anchor long
+  std::vector<int> h_ira;   // secondary primaries | offsets
   std::vector<DecodeItem> h_dwork;
   std::vector<DecodeGroup> h_groups;
   std::vector<int> h_grprow;
@@ -571,6 +581,7 @@ alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* 
   const int d = c.d_model, nf = c.n_feat;
   embed_kernel<T><<<M, 256, 0, st>>>(ctx->at<float>(L.resid), tokens, ctx->at<T>(L.w_embed),
                                      reinterpret_cast<const T*>(embeds), mask, d);
+  keep_tokens_kernel<<<(M + 255) / 256, 256, 0, st>>>(ctx->at<int>(L.i_ctok), tokens, mask, M);
   ALR_LAUNCHED(ctx, "embed");
   for (int l = 0; l < c.n_layers; ++l) {
     const int f = feat_index(c, l);
@@ -587,31 +598,74 @@ alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* 
   return ALR_OK;
 }
 
+// Output destinations of the labels of one rollout or corpus-label call.
+struct LabelDst {
+  float* logprobs;  // [n, block, V] or null (then the logits go to the workspace)
+  int* tokens;      // argmax per slot [n, block]
+  int* top_ids;     // [n, block, 8] or null (no top-8 labels)
+  float* top_logp;
+  float* tail;
+};
+
+// Output head of slot s for the n sorted rows in xnorm: logits GEMM (into the
+// caller's log-prob rows, or the workspace rows when none are wanted), then
+// the finalisation.  `rollout` feeds the next tokens (forced or greedy);
+// otherwise the rows' validity and corpus targets come from the workspace.
 template <typename T>
-alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, int* tokens_out,
-                   float* logprobs_out, hipStream_t st) {
+alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, const LabelDst& out,
+                   bool rollout, float* target_logp, hipStream_t st) {
   const alr_config& c = ctx->cfg;
   const Layout& L = ctx->L;
   const int V = c.vocab, d = c.d_model;
   const int* perm = ctx->at<int>(L.i_perm);
   EpiLogits el;
-  el.out = logprobs_out + (long)s * V;
-  el.rs = (long)block * V;
-  el.perm = perm;
+  LmFinalize f;
+  if (out.logprobs) {
+    el.out = out.logprobs + (long)s * V;
+    el.rs = (long)block * V;
+    el.perm = perm;
+    f.z = out.logprobs + (long)s * V;
+    f.z_rs = (long)block * V;
+    f.z_perm = 1;
+    f.write_lp = 1;
+  } else {
+    el.out = ctx->at<float>(L.logits);
+    el.rs = V;
+    el.perm = nullptr;
+    f.z = ctx->at<float>(L.logits);
+    f.z_rs = V;
+    f.z_perm = 0;
+    f.write_lp = 0;
+  }
   launch_gemm<ALR_PROF_LM_GEMM, T>(ctx, ctx->at<T>(L.xnorm), d, ctx->at<T>(L.w_lm), d, n, V, d,
                                    el, st);
+  f.perm = perm;
+  f.V = V;
+  f.block = block;
+  f.s = s;
+  f.tokens = out.tokens;
+  f.forced = rollout ? forced : nullptr;
+  f.next_tok = rollout ? ctx->at<int>(L.i_cur) : nullptr;
+  f.top_ids = out.top_ids;
+  f.top_logp = out.top_logp;
+  f.tail = out.tail;
+  f.target = rollout ? nullptr : ctx->at<int>(L.i_target);
+  f.target_logp = rollout ? nullptr : target_logp;
+  f.valid = rollout ? nullptr : ctx->at<unsigned char>(L.i_valid);
   {
     ProfScope ps(ctx, ALR_PROF_LM_FINALIZE, st);
-    lm_finalize_kernel<<<n, 256, 0, st>>>(logprobs_out + (long)s * V, (long)block * V, perm, V,
-                                          tokens_out, block, s, forced, ctx->at<int>(L.i_cur));
+    if (out.top_ids)
+      lm_finalize_kernel<true><<<n, 256, 0, st>>>(f);
+    else
+      lm_finalize_kernel<false><<<n, 256, 0, st>>>(f);
   }
   ALR_LAUNCHED(ctx, "output head");
   return ALR_OK;
 }
 
 template <typename T>
-alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, int32_t* tokens_out,
-                        float* logprobs_out, float* feats_out, hipStream_t st) {
+alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, const LabelDst& out,
+                        float* feats_out, hipStream_t st) {
   const alr_config& c = ctx->cfg;
   const Layout& L = ctx->L;
   const int d = c.d_model, nf = c.n_feat;
@@ -623,7 +677,7 @@ alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, i
     gather_feat_kernel<<<n, 256, 0, st>>>(feats_out, (long)block * nf * d, perm,
                                           ctx->at<float>(L.feat_store), atok, (long)nf * d);
   ALR_LAUNCHED(ctx, "slot-0 gather");
-  alr_status stt = lm_head<T>(ctx, n, 0, block, forced, tokens_out, logprobs_out, st);
+  alr_status stt = lm_head<T>(ctx, n, 0, block, forced, out, true, nullptr, st);
   if (stt != ALR_OK) return stt;
   for (int s = 1; s < block; ++s) {
     embed_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<int>(L.i_cur),
@@ -637,9 +691,34 @@ alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, i
     }
     rmsnorm_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
                                          ctx->at<T>(L.xnorm), d, c.rms_eps);
-    stt = lm_head<T>(ctx, n, s, block, forced, tokens_out, logprobs_out, st);
+    stt = lm_head<T>(ctx, n, s, block, forced, out, true, nullptr, st);
     if (stt != ALR_OK) return stt;
   }
+  return ALR_OK;
+}
+
+// Corpus labels: for every slot s, the prefill's final-norm rows at a + s
+// through the output head, the corpus token's log-prob, then the gates.
+template <typename T>
+alr_status corpus_impl(alr_ctx* ctx, int n, int block, const LabelDst& out, float* corpus_logp,
+                       float* gate_soft, float* gate_hard, hipStream_t st) {
+  const alr_config& c = ctx->cfg;
+  const Layout& L = ctx->L;
+  const int d = c.d_model;
+  for (int s = 0; s < block; ++s) {
+    corpus_rows_kernel<T><<<n, 256, 0, st>>>(
+        ctx->at<T>(L.xnorm), ctx->at<T>(L.hf_store), ctx->at<int>(L.i_atok),
+        ctx->at<int>(L.i_apos), ctx->at<int>(L.i_alen), ctx->at<int>(L.i_ctok), s, d,
+        ctx->at<unsigned char>(L.i_valid), ctx->at<int>(L.i_target));
+    ALR_LAUNCHED(ctx, "corpus rows");
+    const alr_status stt = lm_head<T>(ctx, n, s, block, nullptr, out, false, corpus_logp, st);
+    if (stt != ALR_OK) return stt;
+  }
+  erase_gates_kernel<<<(n + 255) / 256, 256, 0, st>>>(
+      ctx->at<int>(L.i_perm), ctx->at<int>(L.i_atok), ctx->at<int>(L.i_apos),
+      ctx->at<int>(L.i_alen), ctx->at<int>(L.i_ctok), corpus_logp, out.tokens, n, block,
+      gate_soft, gate_hard);
+  ALR_LAUNCHED(ctx, "erase gates");
   return ALR_OK;
 }
 
@@ -910,19 +989,19 @@ alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, cons
   return st;
 }
 
-alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
-                       const int32_t* anchor_pos, int32_t block, const int32_t* forced,
-                       int32_t* tokens_out, float* logprobs_out, float* feats_out,
-                       alr_stream stream) {
-  if (!ctx) return ALR_E_INVALID_ARG;
-  if (!ctx->prefilled) return fail(ctx, ALR_E_STATE, "rollout before a successful prefill");
+namespace {
+
+// Validates an anchor request, sorts the anchors by (sequence, position) and
+// uploads the per-anchor tables (and, for a rollout, the decode-attention work
+// split) to the workspace on stream s.
+alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                           const int32_t* anchor_pos, int32_t block, bool rollout,
+                           hipStream_t s) {
+  if (!ctx->prefilled) return fail(ctx, ALR_E_STATE, "call before a successful prefill");
   char msg[256];
   alr_status st = check_rollout_impl(ctx->cfg, ctx->lim, ctx->n_seq, ctx->seq_len.data(), n_anchor,
                                      anchor_seq, anchor_pos, block, msg, sizeof(msg));
   if (st != ALR_OK) return fail(ctx, st, "%s", msg);
-  if (!tokens_out || !logprobs_out)
-    return fail(ctx, ALR_E_INVALID_ARG, "tokens_out and logprobs_out must not be NULL");
-  hipStream_t s = static_cast<hipStream_t>(stream);
   const alr_config& c = ctx->cfg;
   const int n = n_anchor;
   std::vector<int> order(n);
@@ -932,116 +1011,223 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
     if (anchor_pos[x] != anchor_pos[y]) return anchor_pos[x] < anchor_pos[y];
     return x < y;
   });
-  ctx->h_anch.resize((size_t)4 * n);
+  ctx->h_anch.resize((size_t)5 * n);
   int* perm = ctx->h_anch.data();
   int* apos = perm + n;
   int* atok = perm + 2 * n;
   int* aseq = perm + 3 * n;
+  int* alen = perm + 4 * n;
   for (int r = 0; r < n; ++r) {
     const int i = order[r];
     perm[r] = i;
     apos[r] = anchor_pos[i];
     atok[r] = ctx->seq_off[anchor_seq[i]] + anchor_pos[i];
     aseq[r] = ctx->seq_off[anchor_seq[i]];
+    alen[r] = ctx->seq_len[anchor_seq[i]];
   }
   ctx->h_dwork.clear();
   ctx->h_groups.clear();
   ctx->h_grprow.assign(n, 0);
-  if (mfma_attn(c)) {
-    // Groups of up to 128/rep sorted anchors of one sequence.  The shared keys
-    // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
-    // at absolute key positions, so the groups of one sequence read the same
-    // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
-    // dealt so that consecutive items run on one XCD (workgroup b is
-    // dispatched to XCD b % 8): the groups sharing a chunk meet in that L2.
-    const int ag = anchor_group(c), G = c.n_kv_heads;
-    struct Grp {
-      int f, cnt, sq, a_max, ntile;
-    };
-    std::vector<Grp> gs;
-    long total_tiles = 0;
-    for (int r0 = 0; r0 < n;) {
-      const int sq = anchor_seq[order[r0]];
-      int r1 = r0;
-      while (r1 < n && anchor_seq[order[r1]] == sq) ++r1;
-      for (int f = r0; f < r1; f += ag) {
-        const int cnt = std::min(ag, r1 - f);
-        const int a_max = apos[f + cnt - 1];
-        gs.push_back(Grp{f, cnt, sq, a_max, (a_max + AT_KT) / AT_KT});
-        total_tiles += (long)gs.back().ntile * G;
+  if (rollout) {
+    if (mfma_attn(c)) {
+      // Groups of up to 128/rep sorted anchors of one sequence.  The shared keys
+      // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
+      // at absolute key positions, so the groups of one sequence read the same
+      // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
+      // dealt so that consecutive items run on one XCD (workgroup b is
+      // dispatched to XCD b % 8): the groups sharing a chunk meet in that L2.
+      const int ag = anchor_group(c), G = c.n_kv_heads;
+      struct Grp {
+        int f, cnt, sq, a_max, ntile;
+      };
+      std::vector<Grp> gs;
+      long total_tiles = 0;
+      for (int r0 = 0; r0 < n;) {
+        const int sq = anchor_seq[order[r0]];
+        int r1 = r0;
+        while (r1 < n && anchor_seq[order[r1]] == sq) ++r1;
+        for (int f = r0; f < r1; f += ag) {
+          const int cnt = std::min(ag, r1 - f);
+          const int a_max = apos[f + cnt - 1];
+          gs.push_back(Grp{f, cnt, sq, a_max, (a_max + AT_KT) / AT_KT});
+          total_tiles += (long)gs.back().ntile * G;
+        }
+        r0 = r1;
       }
-      r0 = r1;
-    }
-    int max_nt = 1;
-    for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
-    const int ct_min = (int)std::max<long>(
-        AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
-    const long slots = 2L * ctx->n_cu;
-    int ct = std::max(ct_min, max_nt);
-    double best = -1.0;
-    for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
-      long items = 0;
-      for (const Grp& gr : gs) items += (long)((gr.ntile + cand - 1) / cand) * G;
-      const double cost = (double)((items + slots - 1) / slots) * (cand + AT_DECODE_ITEM_OVERHEAD);
-      if (best < 0 || cost < best) {
-        best = cost;
-        ct = cand;
+      int max_nt = 1;
+      for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
+      const int ct_min = (int)std::max<long>(
+          AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
+      const long slots = 2L * ctx->n_cu;
+      int ct = std::max(ct_min, max_nt);
+      double best = -1.0;
+      for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
+        long items = 0;
+        for (const Grp& gr : gs) items += (long)((gr.ntile + cand - 1) / cand) * G;
+        const double cost = (double)((items + slots - 1) / slots) * (cand + AT_DECODE_ITEM_OVERHEAD);
+        if (best < 0 || cost < best) {
+          best = cost;
+          ct = cand;
+        }
       }
-    }
-    int part = 0;
-    for (size_t gi = 0; gi < gs.size(); ++gi) {
-      const int nchunk = (gs[gi].ntile + ct - 1) / ct;
-      ctx->h_groups.push_back(DecodeGroup{gs[gi].f, nchunk, part});
-      for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) ctx->h_grprow[rr] = (int)gi;
-      part += nchunk * G;
-    }
-    std::vector<DecodeItem> logical;
-    for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
-      size_t g1 = g0;
-      int max_chunks = 0;
-      while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
-        max_chunks = std::max(max_chunks, ctx->h_groups[g1].nchunk);
-        ++g1;
+      int part = 0;
+      for (size_t gi = 0; gi < gs.size(); ++gi) {
+        const int nchunk = (gs[gi].ntile + ct - 1) / ct;
+        ctx->h_groups.push_back(DecodeGroup{gs[gi].f, nchunk, part});
+        for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) ctx->h_grprow[rr] = (int)gi;
+        part += nchunk * G;
       }
-      const int sq = gs[g0].sq;
-      for (int g = 0; g < G; ++g)
-        for (int ch = 0; ch < max_chunks; ++ch)
-          for (size_t gi = g0; gi < g1; ++gi) {
-            const DecodeGroup& dg = ctx->h_groups[gi];
-            if (ch >= dg.nchunk) continue;
-            const int kb = ch * ct * AT_KT;
-            const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
-            logical.push_back(DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[sq],
-                                         ctx->seq_vcol[sq], kb, ke, dg.part0 + g * dg.nchunk + ch});
-          }
-      g0 = g1;
-    }
-    const size_t per = (logical.size() + 7) / 8;
-    ctx->h_dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
-    for (size_t b = 0; b < per * 8; ++b) {
-      const size_t li = (b % 8) * per + b / 8;
-      if (li < logical.size()) ctx->h_dwork[b] = logical[li];
+      std::vector<DecodeItem> logical;
+      for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
+        size_t g1 = g0;
+        int max_chunks = 0;
+        while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
+          max_chunks = std::max(max_chunks, ctx->h_groups[g1].nchunk);
+          ++g1;
+        }
+        const int sq = gs[g0].sq;
+        for (int g = 0; g < G; ++g)
+          for (int ch = 0; ch < max_chunks; ++ch)
+            for (size_t gi = g0; gi < g1; ++gi) {
+              const DecodeGroup& dg = ctx->h_groups[gi];
+              if (ch >= dg.nchunk) continue;
+              const int kb = ch * ct * AT_KT;
+              const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
+              logical.push_back(DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[sq],
+                                           ctx->seq_vcol[sq], kb, ke, dg.part0 + g * dg.nchunk + ch});
+            }
+        g0 = g1;
+      }
+      const size_t per = (logical.size() + 7) / 8;
+      ctx->h_dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
+      for (size_t b = 0; b < per * 8; ++b) {
+        const size_t li = (b % 8) * per + b / 8;
+        if (li < logical.size()) ctx->h_dwork[b] = logical[li];
+      }
     }
   }
   if (ctx->h_dwork.size() > ctx->L.max_dwork || ctx->h_groups.size() > ctx->L.max_groups)
     return fail(ctx, ALR_E_WORKSPACE, "decode work list overflow");
   const Layout& L = ctx->L;
-  // perm, apos, atok, aseq live in consecutive workspace arrays of max_anchors each
   st = upload(ctx, ctx->at<int>(L.i_perm), perm, (size_t)n * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_apos), apos, (size_t)n * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_atok), atok, (size_t)n * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_aseq), aseq, (size_t)n * 4, s);
-  if (st == ALR_OK)
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_alen), alen, (size_t)n * 4, s);
+  if (st == ALR_OK && !ctx->h_dwork.empty())
     st = upload(ctx, ctx->at<DecodeItem>(L.i_dwork), ctx->h_dwork.data(),
                 ctx->h_dwork.size() * sizeof(DecodeItem), s);
-  if (st == ALR_OK)
+  if (st == ALR_OK && !ctx->h_groups.empty())
     st = upload(ctx, ctx->at<DecodeGroup>(L.i_groups), ctx->h_groups.data(),
                 ctx->h_groups.size() * sizeof(DecodeGroup), s);
-  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_grprow), ctx->h_grprow.data(), (size_t)n * 4, s);
+  if (st == ALR_OK && rollout)
+    st = upload(ctx, ctx->at<int>(L.i_grprow), ctx->h_grprow.data(), (size_t)n * 4, s);
+  return st;
+}
+
+}  // namespace
+
+alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                       const int32_t* anchor_pos, int32_t block, const int32_t* forced,
+                       int32_t* tokens_out, float* logprobs_out, float* feats_out,
+                       alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (!tokens_out || !logprobs_out)
+    return fail(ctx, ALR_E_INVALID_ARG, "tokens_out and logprobs_out must not be NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  alr_status st = prepare_anchors(ctx, n_anchor, anchor_seq, anchor_pos, block, true, s);
   if (st != ALR_OK) return st;
-  return (c.dtype == ALR_BF16)
-             ? rollout_impl<bf16>(ctx, n, block, forced, tokens_out, logprobs_out, feats_out, s)
-             : rollout_impl<float>(ctx, n, block, forced, tokens_out, logprobs_out, feats_out, s);
+  const LabelDst out{logprobs_out, tokens_out, nullptr, nullptr, nullptr};
+  return (ctx->cfg.dtype == ALR_BF16)
+             ? rollout_impl<bf16>(ctx, n_anchor, block, forced, out, feats_out, s)
+             : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
+}
+
+alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                            const int32_t* anchor_pos, int32_t block, const int32_t* forced,
+                            int32_t* tokens_out, int32_t* top_ids_out, float* top_logp_out,
+                            float* tail_out, float* logprobs_out, float* feats_out,
+                            alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (!tokens_out || !top_ids_out || !top_logp_out || !tail_out)
+    return fail(ctx, ALR_E_INVALID_ARG,
+                "tokens_out, top_ids_out, top_logp_out and tail_out must not be NULL");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  alr_status st = prepare_anchors(ctx, n_anchor, anchor_seq, anchor_pos, block, true, s);
+  if (st != ALR_OK) return st;
+  const LabelDst out{logprobs_out, tokens_out, top_ids_out, top_logp_out, tail_out};
+  return (ctx->cfg.dtype == ALR_BF16)
+             ? rollout_impl<bf16>(ctx, n_anchor, block, forced, out, feats_out, s)
+             : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
+}
+
+alr_status alr_corpus_labels(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                             const int32_t* anchor_pos, int32_t block, int32_t* argmax_out,
+                             int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                             float* logprobs_out, float* corpus_logp_out, float* gate_soft_out,
+                             float* gate_hard_out, alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (!argmax_out || !corpus_logp_out || !gate_soft_out || !gate_hard_out)
+    return fail(ctx, ALR_E_INVALID_ARG,
+                "argmax_out, corpus_logp_out, gate_soft_out and gate_hard_out must not be NULL");
+  if ((top_ids_out == nullptr) != (top_logp_out == nullptr) ||
+      (top_ids_out == nullptr) != (tail_out == nullptr))
+    return fail(ctx, ALR_E_INVALID_ARG,
+                "top_ids_out, top_logp_out and tail_out must all be given or all be NULL");
+  if (!top_ids_out && !logprobs_out)
+    return fail(ctx, ALR_E_INVALID_ARG, "give top-8 outputs, log-prob rows or both");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  alr_status st = prepare_anchors(ctx, n_anchor, anchor_seq, anchor_pos, block, false, s);
+  if (st != ALR_OK) return st;
+  const LabelDst out{logprobs_out, argmax_out, top_ids_out, top_logp_out, tail_out};
+  return (ctx->cfg.dtype == ALR_BF16)
+             ? corpus_impl<bf16>(ctx, n_anchor, block, out, corpus_logp_out, gate_soft_out,
+                                 gate_hard_out, s)
+             : corpus_impl<float>(ctx, n_anchor, block, out, corpus_logp_out, gate_soft_out,
+                                  gate_hard_out, s);
+}
+
+alr_status alr_ira_assemble(alr_ctx* ctx, int32_t n_primary, int32_t block,
+                            const int32_t* tokens, const int32_t* top_ids, const float* top_logp,
+                            const float* tail, int32_t n_secondary, const int32_t* sec_primary,
+                            const int32_t* sec_offset, float gamma, int32_t* token0_out,
+                            int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                            float* weight_out, alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (n_primary <= 0 || n_primary > ctx->lim.max_anchors || block < 2 ||
+      block > ctx->lim.max_block)
+    return fail(ctx, ALR_E_INVALID_ARG, "n_primary %d / block %d outside the context limits",
+                n_primary, block);
+  if (n_secondary < 0 || n_secondary > ctx->lim.max_anchors)
+    return fail(ctx, ALR_E_INVALID_ARG, "n_secondary %d outside [0, %d]", n_secondary,
+                ctx->lim.max_anchors);
+  if (!(gamma > 0.f)) return fail(ctx, ALR_E_INVALID_ARG, "gamma must be > 0");
+  if (n_secondary == 0) return ALR_OK;
+  if (!tokens || !top_ids || !top_logp || !tail || !sec_primary || !sec_offset || !token0_out ||
+      !top_ids_out || !top_logp_out || !tail_out || !weight_out)
+    return fail(ctx, ALR_E_INVALID_ARG, "NULL pointer argument");
+  std::vector<int>& tab = ctx->h_ira;  // kept until the next call: the copy is asynchronous
+  tab.assign((size_t)2 * n_secondary, 0);
+  for (int q = 0; q < n_secondary; ++q) {
+    if (sec_primary[q] < 0 || sec_primary[q] >= n_primary)
+      return fail(ctx, ALR_E_OUT_OF_RANGE, "secondary %d: primary %d outside [0, %d)", q,
+                  sec_primary[q], n_primary);
+    if (sec_offset[q] < 1 || sec_offset[q] > block - 1)
+      return fail(ctx, ALR_E_OUT_OF_RANGE, "secondary %d: offset %d outside [1, %d]", q,
+                  sec_offset[q], block - 1);
+    tab[q] = sec_primary[q];
+    tab[n_secondary + q] = sec_offset[q];
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int* dtab = ctx->at<int>(ctx->L.i_ira);
+  const alr_status st = upload(ctx, dtab, tab.data(), tab.size() * 4, s);
+  if (st != ALR_OK) return st;
+  const long items = (long)n_secondary * block;
+  ira_assemble_kernel<<<(unsigned)((items + 255) / 256), 256, 0, s>>>(
+      dtab, dtab + n_secondary, n_secondary, block, tokens, top_ids, top_logp, tail, gamma,
+      token0_out, top_ids_out, top_logp_out, tail_out, weight_out);
+  ALR_LAUNCHED(ctx, "in-rollout anchor assembly");
+  return ALR_OK;
 }
 
 const char* alr_last_error(const alr_ctx* ctx) {
