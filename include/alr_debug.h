@@ -29,10 +29,14 @@ extern "C" {
  * 5 stages), 13 = 256x256 (4 waves, 4 stages), 14 = 128x128 (4 stages);
  * ping-pong (the two waves of each SIMD alternate LDS/transfer and MFMA
  * phases): 15 = 256x256 (4 stages), 16 = 256x256 (5 stages); 17 = ping-pong
- * over register-staged BK = 64 tiles (K a multiple of 64).  Tiles 6..8 need a device scratch buffer of
- * N*K*2 + N*8 bytes (ALR_E_WORKSPACE otherwise) to hold the pre-shuffled W;
- * the call then synchronises `stream` once after shuffling.  Enqueued on
- * `stream`. */
+ * over register-staged BK = 64 tiles (K a multiple of 64); 18 = split-K over
+ * the ping-pong kernel (K slices summed in slice order by a second kernel;
+ * 2 or 4 slices by the library's rule, at least 2; K a multiple of 128).
+ * Tiles 6..8 need a device scratch buffer of N*K*2 + N*8 bytes to hold the
+ * pre-shuffled W (the call then synchronises `stream` once after
+ * shuffling); tile 18 needs one of at least 2*M*N*4 bytes for the partial
+ * sums (up to 4*M*N*4 are used when given); ALR_E_WORKSPACE otherwise.
+ * Enqueued on `stream`. */
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
                           int32_t N, int32_t K, int32_t tile, void* scratch,
                           size_t scratch_bytes, alr_stream stream);

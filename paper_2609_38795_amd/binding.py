@@ -382,6 +382,9 @@ def debug_gemm(dtype: int, A, W, C, stream=None, tile: int = 0):
     if dtype == ALR_BF16 and 6 <= tile <= 8:
         nbytes = N * K * 2 + N * 8
         scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
+    if dtype == ALR_BF16 and tile == 18:
+        nbytes = 4 * M * N * 4
+        scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
     st = lib.alr_debug_gemm(dtype, A.data_ptr(), W.data_ptr(), C.data_ptr(), M, N, K, tile,
                             None if scratch is None else scratch.data_ptr(), nbytes,
                             ctypes.c_void_p(s.cuda_stream))

@@ -66,7 +66,36 @@ struct EpiQKV {
       Elt<OutT>::st(dst + cl + 32, hi);
     }
   }
+  // Rows row0 .. row0+nrow-1 (nrow <= 4) of columns c and c+32.  Four rows
+  // that are four consecutive, 4-aligned columns of the transposed V cache go
+  // out as one 8-byte store per column (bf16); everything else per element.
+  __device__ __forceinline__ void quad(int row0, int nrow, int c, const float* lo,
+                                       const float* hi) const {
+    if constexpr (std::is_same<OutT, bf16>::value) {
+      if (vt_col && c >= (H + G) * hd && nrow == 4) {
+        const int col0 = vt_col[row0];
+        if (vt_col[row0 + 3] == col0 + 3 && (col0 & 3) == 0) {
+          const long cl = c - (H + G) * hd;
+          u32x2 wl, wh;
+          wl[0] = pack2bf(lo[0], lo[1]);
+          wl[1] = pack2bf(lo[2], lo[3]);
+          wh[0] = pack2bf(hi[0], hi[1]);
+          wh[1] = pack2bf(hi[2], hi[3]);
+          *(u32x2*)(v + cl * vt_stride + col0) = wl;
+          *(u32x2*)(v + (cl + 32) * vt_stride + col0) = wh;
+          return;
+        }
+      }
+    }
+    for (int i = 0; i < nrow; ++i) (*this)(row0 + i, c, lo[i], hi[i]);
+  }
 };
+
+// Epilogues that handle four rows of a column pair at once define quad().
+template <class Epi, class = void>
+struct has_quad : std::false_type {};
+template <class Epi>
+struct has_quad<Epi, decltype((void)&Epi::quad)> : std::true_type {};
 
 // Residual add into the fp32 stream, optionally capturing the new value as a
 // feature row: feat + (perm ? perm[row] : row) * feat_rs.
@@ -116,6 +145,84 @@ struct EpiLogits {
   }
 };
 
+// Epilogue of a wave's MI x NI block of 32x32 accumulators whose top-left
+// output is (row0, col0): lane (lr, lh) of block (mi, nj) holds rows row0 +
+// 32 mi + 8 q + 4 lh + e (q, e = 0..3; register 4 q + e) of columns col0 +
+// 64 nj + lr and that + 32 (accumulators 2 nj and 2 nj + 1).
+template <int MI, int NI, class Epi>
+__device__ __forceinline__ void gemm_store_tile(const Epi& epi, const f32x16 (&acc)[MI][NI],
+                                                int row0, int col0, int M, int N) {
+  const int lane = threadIdx.x & 63, lr = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int nj = 0; nj < NI / 2; ++nj) {
+    const int col = col0 + nj * 64 + lr;
+    if (col < N) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = row0 + mi * 32 + 8 * q + 4 * lh;
+          if constexpr (has_quad<Epi>::value) {
+            if (row < M) {
+              float lo[4], hi[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                lo[e] = acc[mi][2 * nj][4 * q + e];
+                hi[e] = acc[mi][2 * nj + 1][4 * q + e];
+              }
+              epi.quad(row, min(4, M - row), col, lo, hi);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (row + e < M) epi(row + e, col, acc[mi][2 * nj][4 * q + e], acc[mi][2 * nj + 1][4 * q + e]);
+          }
+        }
+    }
+  }
+}
+
+// Split-K: slice s of the K range writes raw fp32 sums of columns c and c+32
+// to out + s * sstride + row * ld; splitk_reduce_kernel adds the slices in
+// slice order (the result does not depend on which slice finished first) and
+// applies the real epilogue.
+struct EpiPartial {
+  float* out;
+  long sstride;
+  int ld;
+  __device__ __forceinline__ void set_split(int sl) { out += sl * sstride; }
+  __device__ __forceinline__ void operator()(int row, int c, float lo, float hi) const {
+    out[(long)row * ld + c] = lo;
+    out[(long)row * ld + c + 32] = hi;
+  }
+};
+
+template <class Epi, class = void>
+struct has_set_split : std::false_type {};
+template <class Epi>
+struct has_set_split<Epi, decltype((void)&Epi::set_split)> : std::true_type {};
+
+// One thread per (row, column c in the low half of a 64-column group).
+template <class Epi>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
+                                                            long sstride, int slices, int M,
+                                                            int N, Epi epi) {
+  const long t = (long)blockIdx.x * 256 + threadIdx.x;
+  const int groups = N / 64;
+  if (t >= (long)M * groups * 32) return;
+  const int c32 = (int)(t & 31);
+  const long rg = t >> 5;
+  const int g = (int)(rg % groups), row = (int)(rg / groups);
+  const int col = g * 64 + c32;
+  const float* p = part + (long)row * N + col;
+  float lo = 0.f, hi = 0.f;
+  for (int sl = 0; sl < slices; ++sl) {
+    lo += p[sl * sstride];
+    hi += p[sl * sstride + 32];
+  }
+  epi(row, col, lo, hi);
+}
+
 // ------------------------------------------------------------------ bf16 MFMA GEMM
 //
 // Workgroup tile BM x BN, WGM x WGN waves, wave tile (BM/WGM) x (BN/WGN) with a
@@ -134,9 +241,9 @@ struct EpiLogits {
 // block id is first remapped to make each XCD walk a contiguous range of the
 // tile order; the order itself groups 8 M-tiles per N sweep so neighbouring
 // tiles share A rows and W rows in L2.
-__device__ __forceinline__ void gemm_tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ void gemm_tile_coords(int bid, int tiles_m, int tiles_n, int& tm,
+                                                 int& tn) {
   const int nb = tiles_m * tiles_n;
-  int bid = blockIdx.x;
   if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
   const int group = 8;
   const int per_group = group * tiles_n;
@@ -146,6 +253,9 @@ __device__ __forceinline__ void gemm_tile_coords(int tiles_m, int tiles_n, int& 
   const int in = bid - g * per_group;
   tm = first_m + in % gm;
   tn = in / gm;
+}
+__device__ __forceinline__ void gemm_tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  gemm_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
 }
 
 // Element offset of 16-byte chunk c of LDS row r for rows of BK bf16.
@@ -324,20 +434,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
     __syncthreads();
   }
 
-  const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS ring
@@ -487,20 +584,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_dma_kernel(
   }
   wait_vmcnt<0>();  // no transfer may still target this workgroup's LDS
 
-  const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, ping-pong
@@ -606,20 +690,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(
   if (grp == 0) __builtin_amdgcn_s_barrier();
   wait_vmcnt<0>();  // no transfer may still target this workgroup's LDS
 
-  const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, ping-pong, BK = 64
@@ -637,17 +708,30 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(
 // rewritten only after both groups finished reading it (the barrier after the
 // last memory phase of step s-1).  Each memory phase ends with its LDS work
 // complete, so the barrier publishes the writes.
+// With splits > 1 the grid holds `splits` workgroups per tile: workgroup b
+// computes K slice b % splits (K is then the slice length; A and W advance by
+// slice * K columns) of tile b / splits, for an epilogue with set_split.
 template <int TAG, class Epi>
 __global__ __launch_bounds__(512, 1) void gemm_bf16_pp64_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
+    int tiles_m, int tiles_n, Epi epi, int splits = 1) {
   constexpr int BM = 256, BN = 256, BK = 64;
   constexpr int WTM = 128, WTN = 64, MI = 4, NI = 2;
   constexpr int STAGE = (BM + BN) * BK;  // bf16 elements
   __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STAGE];
 
+  int bid = blockIdx.x;
+  if constexpr (has_set_split<Epi>::value) {
+    if (splits > 1) {
+      const int sl = bid % splits;
+      bid /= splits;
+      A += (long)sl * K;
+      W += (long)sl * K;
+      epi.set_split(sl);
+    }
+  }
   int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
+  gemm_tile_coords(bid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -723,20 +807,7 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp64_kernel(
   }
   if (grp == 0) __builtin_amdgcn_s_barrier();
 
-  const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, 3-stage LDS ring
@@ -861,20 +932,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_r3_kernel(
     s = (s == 2) ? 0 : s + 1;
   }
 
-  const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, W in registers
@@ -1023,19 +1081,7 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_wd_kernel(
     __syncthreads();
   }
 
-#pragma unroll
-  for (int nj = 0; nj < NI / 2; ++nj) {
-    const int col = n0 + wn * WTN + nj * 64 + lr;
-    if (col < N) {
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WTM + mi * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (row < M) epi(row, col, acc[mi][2 * nj][r], acc[mi][2 * nj + 1][r]);
-        }
-    }
-  }
+  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ fp32 FMA GEMM

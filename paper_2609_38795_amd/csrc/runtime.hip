@@ -54,6 +54,7 @@ struct Layout {
   size_t i_valid, i_target, i_ira, i_ctok, logits;
   size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
+  size_t splitk, splitk_bytes;
   size_t max_pwork, max_dwork, max_groups;
   size_t total;
 };
@@ -199,6 +200,9 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_grprow = take(NA * 4);
   L.part_o = take(L.max_dwork * 128 * hd * 4);
   L.part_ml = take(L.max_dwork * 128 * 2 * 4);
+  // split-K partial sums of the rollout GEMMs: up to 4 slices of [anchors, N] fp32
+  L.splitk_bytes = 4 * NA * std::max(qd + 2 * kvd, d) * 4;
+  L.splitk = take(L.splitk_bytes);
   L.total = off;
   return off;
 }
@@ -261,6 +265,8 @@ struct alr_ctx {
   Layout L;
   bool prefilled = false;
   int n_cu = 256;  // compute units of the device (sizes the decode work split)
+  float* splitk_buf = nullptr;  // split-K partial sums (workspace)
+  size_t splitk_bytes = 0;
   int n_seq = 0;
   std::vector<int> seq_len, seq_off;
   std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
@@ -336,6 +342,29 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     // pre-shuffled.
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     int cfg = force_tile;
+    // Split-K over the 256x256 ping-pong kernel when its tiles leave CUs idle:
+    // the largest slice count in {2, 4} that keeps one workgroup per CU, K
+    // slices of >= 512 and a multiple of 64, and the partial sums in the buffer.
+    if ((cfg == 0 || cfg == 18) && ctx->splitk_buf != nullptr) {
+      const int t256 = tiles(256, 256);
+      int S = 1;
+      for (int cand : {2, 4})
+        if ((long)t256 * cand <= ctx->n_cu && K % (64 * cand) == 0 && K / cand >= 512 &&
+            (size_t)cand * M * N * 4 <= ctx->splitk_bytes)
+          S = cand;
+      if (cfg == 18 && S == 1 && K % 128 == 0 && (size_t)2 * M * N * 4 <= ctx->splitk_bytes) S = 2;
+      if (S > 1 && (cfg == 18 || t256 < ctx->n_cu)) {
+        const int tm = (M + 255) / 256, tn = (N + 255) / 256;
+        EpiPartial ep{ctx->splitk_buf, (long)M * N, N};
+        gemm_bf16_pp64_kernel<TAG, EpiPartial>
+            <<<t256 * S, 512, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
+        const long thr = (long)M * (N / 64) * 32;
+        splitk_reduce_kernel<Epi>
+            <<<(unsigned)((thr + 255) / 256), 256, 0, st>>>(ctx->splitk_buf, (long)M * N, S, M, N, epi);
+        return;
+      }
+      if (cfg == 18) cfg = 0;
+    }
     if (cfg == 0)
       cfg = tiles(256, 256) >= 256 ? ((K % 64) == 0 ? 17 : 4) : (tiles(128, 128) >= 256 ? 2 : 3);
     // the direct-to-LDS kernels address operands with 32-bit byte offsets
@@ -826,6 +855,8 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
     CREATE_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
     ctx->n_cu = std::max(1, ncu);
   }
+  ctx->splitk_buf = ctx->at<float>(L.splitk);
+  ctx->splitk_bytes = L.splitk_bytes;
   const size_t es = L.es, d = c.d_model, F = c.d_ffn, V = c.vocab;
   const int H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
   const size_t qd = (size_t)H * hd, kvd = (size_t)G * hd;
@@ -1247,7 +1278,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || tile > 17) return ALR_E_INVALID_ARG;
+  if (tile < 0 || tile > 18) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
@@ -1270,6 +1301,11 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
           static_cast<bf16*>(scratch), drp, N, K);
       if (hipStreamSynchronize(s) != hipSuccess) return ALR_E_HIP;
       Wk = static_cast<const bf16*>(scratch);
+    }
+    if (tile == 18) {  // split-K: partial sums in the scratch buffer
+      if (!scratch || scratch_bytes < (size_t)2 * M * N * 4) return ALR_E_WORKSPACE;
+      dummy.splitk_buf = static_cast<float*>(scratch);
+      dummy.splitk_bytes = scratch_bytes;
     }
     launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, Wk, K, M, N, K, el, s, tile);
   } else if (dtype == ALR_F32) {
