@@ -28,8 +28,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def site_work(site: str, w) -> dict:
+def site_work(site: str, w, anchor_seq=None, anchor_pos=None) -> dict:
     """Algorithmic FLOPs (or bytes) of one launch at a profiled site."""
+    w_anchor_seq, w_anchor_pos = anchor_seq, anchor_pos
     s = w.shape
     d, F, V = s.d_model, s.d_ffn, s.vocab
     qd, kvd = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
@@ -44,6 +45,18 @@ def site_work(site: str, w) -> dict:
     if site == "lm_finalize":
         # one fp32 read (max/argmax/sum-exp pass) and one read+write (log-softmax) per entry
         return {"bound": "hbm", "bytes": 12.0 * NA * V, "unit": "GB/s"}
+    if site == "decode_attn":
+        # unique bytes of one launch, averaged over the rollout steps s = 1 .. B-1: every
+        # sequence's shared K and V up to its last anchor, each anchor's s private keys and
+        # values, the queries read and the outputs written (bf16)
+        hd, G, H = s.head_dim, s.n_kv_heads, s.n_heads
+        a_max = [int(w_anchor_pos[w_anchor_seq == q].max()) for q in range(w.n_seq)
+                 if (w_anchor_seq == q).any()]
+        shared = sum(a + 1 for a in a_max) * G * hd * 2 * 2
+        steps = max(w.block - 1, 1)
+        private = NA * G * hd * 2 * 2 * (sum(range(1, w.block)) / steps)
+        qo = 2 * NA * H * hd * 2
+        return {"bound": "hbm", "bytes": float(shared + private + qo), "unit": "GB/s"}
     if site == "prefill_attn":
         # causal: sum over positions of 4 * hd * (t+1) per head
         L = w.seq_len
@@ -146,6 +159,8 @@ def main():
     ap.add_argument("--site", default="prefill_gu", help="kernel launch site for the roofline")
     ap.add_argument("--breakdown", action="store_true", help="time every launch site (extra steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the HBM-kernel timing steps (decode attention, output-head finalisation)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -225,7 +240,7 @@ def main():
     value = slots / (ms_per_step / 1e3)
     log(f"[bench] {args.steps} steps: {ms_per_step:.1f} ms/step, {value:.0f} slots/s")
 
-    work = site_work(args.site, w)
+    work = site_work(args.site, w, inp.anchor_seq, inp.anchor_pos)
     avg_s = site_ms / max(site_n, 1) / 1e3
     if work["bound"] == "mfma":
         achieved = work["flops"] / avg_s / 1e12
@@ -238,6 +253,23 @@ def main():
                 "traffic": measured_traffic(args.site),
                 "kernel": args.site, "avg_launch_ms": round(avg_s * 1e3, 4),
                 "launches_timed": site_n}
+
+    # HBM-side kernels the method also names (decode attention, output-head finalisation):
+    # average launch time over one extra untimed step each, HIP events on the launch stream
+    secondary = []
+    for site2 in (() if args.no_secondary else ("decode_attn", "lm_finalize")):
+        if site2 == args.site:
+            continue
+        binding.profile_start(eng, site2, 1024)
+        step()
+        ms2, n2 = binding.profile_stop(eng)
+        wk2 = site_work(site2, w, inp.anchor_seq, inp.anchor_pos)
+        gbs = wk2["bytes"] / (ms2 / max(n2, 1) / 1e3) / 1e9
+        secondary.append({"kernel": site2, "bound": "hbm", "achieved": round(gbs, 1),
+                          "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                          "avg_launch_ms": round(ms2 / max(n2, 1), 4), "launches_timed": n2,
+                          "bytes_per_launch": wk2["bytes"]})
+        log(f"[bench] {site2}: {gbs:.0f} GB/s of algorithmic bytes ({ms2 / max(n2, 1):.4f} ms/launch)")
 
     if args.copy_calibration:
         n = 1 << 28  # 2^28 fp32 = 1 GiB read + 1 GiB written per launch
@@ -268,6 +300,7 @@ def main():
         "phases_ms": {"prefill": round(prefill_ms, 2), "rollout": round(rollout_ms, 2),
                       "rollout_only_slots_per_s": round(slots / (rollout_ms / 1e3), 1)},
         "roofline": roofline,
+        "roofline_hbm_kernels": secondary,
         "cpu_baseline": cpu,
     }
     if breakdown:
