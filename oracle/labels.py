@@ -17,6 +17,9 @@ What is computed:
   erase objective (Eq. 2): the soft gate ``g_{a,k} = prod_{1<=j<k}
   p_T(x_{a+j} | x_{<a+j})`` and the hard gate, whose factors are the
   indicators ``1[x_{a+j} = argmax p_T(. | x_{<a+j})]``.
+* :func:`slot_weights` -- the slot weights of ALR blocks: ``w_k`` on active
+  slots, 0 on the slots that follow an early end of the rollout (Sec. 3.2: a
+  slot is masked once an end-of-sequence token was fed before it).
 * :func:`ira_secondary` -- the secondary blocks of in-rollout anchors (Sec. 3.2,
   Eq. 4): a block placed at offset ``j`` inside a primary rollout takes the
   target-generated token ``y*_j`` as its slot 0, inherits the primary label at
@@ -65,6 +68,25 @@ def slot_envelope(n_slots: int, gamma: float = 2.0) -> np.ndarray:
     """w_k = exp(-(k-1)/gamma) for k = 1 .. n_slots (Eq. 1), as an array indexed by k-1."""
     k = np.arange(1, n_slots + 1, dtype=np.float64)
     return np.exp(-(k - 1.0) / gamma)
+
+
+def active_slots(tokens, eos_id: Optional[int]) -> np.ndarray:
+    """active[i, s]: no end-of-sequence token among tokens[i, 0 .. s-1] (the tokens fed
+    before index s; index s of a block is the paper's slot s+1).  eos_id None: all active."""
+    tokens = np.asarray(tokens)
+    act = np.ones(tokens.shape, bool)
+    if eos_id is None or eos_id < 0:
+        return act
+    for i in range(tokens.shape[0]):
+        for s in range(1, tokens.shape[1]):
+            act[i, s] = act[i, s - 1] and int(tokens[i, s - 1]) != eos_id
+    return act
+
+
+def slot_weights(tokens, eos_id: Optional[int], gamma: float = 2.0) -> np.ndarray:
+    """omega[i, s] = w_{s+1} on active slots, 0 after an early end (Eq. 1, Sec. 3.2)."""
+    tokens = np.asarray(tokens)
+    return slot_envelope(tokens.shape[1], gamma)[None, :] * active_slots(tokens, eos_id)
 
 
 def corpus_labels(lp_seq: np.ndarray, tokens_seq: np.ndarray, anchor_pos, block: int,
@@ -118,7 +140,8 @@ def corpus_labels(lp_seq: np.ndarray, tokens_seq: np.ndarray, anchor_pos, block:
     return valid, labels, amax, clp, g_soft, g_hard
 
 
-def ira_secondary(tokens, labels, primary, offset, gamma: float = 2.0):
+def ira_secondary(tokens, labels, primary, offset, gamma: float = 2.0,
+                  eos_id: Optional[int] = None):
     """Secondary blocks of in-rollout anchors (Eq. 4).
 
     tokens[n_prim, B]: the primary rollouts' greedy tokens (index s holds
@@ -129,7 +152,9 @@ def ira_secondary(tokens, labels, primary, offset, gamma: float = 2.0):
     Secondary index s' (paper slot k = s'+1) inherits the primary label at
     paper slot j+k, i.e. primary index j+s', where that exists (j+s' <= B-1;
     else the entry is left as fill).  Its weight is w_k 1[j+k <= K] with
-    K = B-1.  Slot 0's token is y*_j = tokens[p, j-1]; the block's slot 0 sits
+    K = B-1, and 0 where the primary had ended before the inherited slot
+    (an end-of-sequence token among tokens[p, 0 .. j+s'-1], with eos_id).
+    Slot 0's token is y*_j = tokens[p, j-1]; the block's slot 0 sits
     at position a + j, so its context is the prefix up to a and the rollout
     positions a+1 .. a+j-1.
 
@@ -143,6 +168,7 @@ def ira_secondary(tokens, labels, primary, offset, gamma: float = 2.0):
     B = tokens.shape[1]
     K = B - 1
     w = slot_envelope(B, gamma)
+    act = active_slots(tokens, eos_id)
     fill = -1 if np.issubdtype(labels.dtype, np.integer) else -np.inf
     out = np.full((n_sec,) + labels.shape[1:], fill, dtype=labels.dtype)
     weight = np.zeros((n_sec, B))
@@ -154,5 +180,6 @@ def ira_secondary(tokens, labels, primary, offset, gamma: float = 2.0):
             k = s2 + 1
             if j + s2 <= B - 1:
                 out[q, s2] = labels[p, j + s2]
-            weight[q, s2] = w[k - 1] if j + k <= K else 0.0
+            alive = j + s2 <= B - 1 and bool(act[p, j + s2])
+            weight[q, s2] = w[k - 1] if (j + k <= K and alive) else 0.0
     return token0, out, weight, np.asarray(offset, np.int64)

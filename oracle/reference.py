@@ -137,13 +137,35 @@ def rope_angles(positions: np.ndarray, head_dim: int, base: float, dt=np.float64
     return np.cos(ang).astype(dt), np.sin(ang).astype(dt)
 
 
-def rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
-    """Rotate-half RoPE on x[T, n_heads, head_dim]: pair (i, i+hd/2) rotates by pos*theta_i."""
+def rope_axis_of(half: int, sections) -> np.ndarray:
+    """Position axis (0 = t, 1 = h, 2 = w) that drives frequency i < half under M-RoPE.
+
+    Multimodal RoPE splits the frequency list into consecutive sections, one per
+    position axis; sections (s_t, s_h, s_w) sum to head_dim / 2.  No sections
+    (None or all zero) means one axis (plain RoPE).
+    """
+    if sections is None or sum(sections) == 0:
+        return np.zeros(half, np.int64)
+    assert sum(sections) == half, (sections, half)
+    return np.repeat(np.arange(3), np.asarray(sections, dtype=np.int64))
+
+
+def rope(x: np.ndarray, positions: np.ndarray, base: float, sections=None) -> np.ndarray:
+    """Rotate-half RoPE on x[T, n_heads, head_dim]: pair (i, i+hd/2) rotates by pos*theta_i.
+
+    positions[T] (one axis) or positions[T, 3] (t, h, w); with sections, frequency i
+    takes the position of its axis (M-RoPE), else axis 0.
+    """
     hd = x.shape[-1]
     half = hd // 2
-    cos, sin = rope_angles(positions, hd, base, x.dtype)
-    cos = cos[:, None, :]
-    sin = sin[:, None, :]
+    pos = np.asarray(positions, dtype=np.float64)
+    if pos.ndim == 1:
+        pos = pos[:, None]
+    axis = rope_axis_of(half, sections)
+    inv = np.power(float(base), -2.0 * np.arange(half, dtype=np.float64) / hd)
+    ang = pos[:, axis] * inv[None, :]  # [T, half]: frequency i at its axis' position
+    cos = np.cos(ang).astype(x.dtype)[:, None, :]
+    sin = np.sin(ang).astype(x.dtype)[:, None, :]
     x1, x2 = x[..., :half], x[..., half:]
     return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
 
@@ -211,8 +233,8 @@ def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
         q = (n1 @ P.get("wq", layer).T).reshape(T, H, hd)
         k = (n1 @ P.get("wk", layer).T).reshape(T, G, hd)
         v = (n1 @ P.get("wv", layer).T).reshape(T, G, hd)
-        q = rnd(rope(q, positions, shape.rope_base))
-        k = rnd(rope(k, positions, shape.rope_base))
+        q = rnd(rope(q, positions, shape.rope_base, _sections(shape)))
+        k = rnd(rope(k, positions, shape.rope_base, _sections(shape)))
         v = rnd(v)
         o = rnd(causal_gqa_attention(q, k, v).reshape(T, H * hd))
         h = h + o @ P.get("wo", layer).T
@@ -223,6 +245,25 @@ def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
             outs.append(h.copy())
     hf = rnd(rmsnorm(h, P.get("final_norm"), eps))
     return outs, hf
+
+
+def _sections(shape):
+    return getattr(shape, "mrope_sections", None)
+
+
+def slot_positions(pos_seq: Optional[np.ndarray], a: int, n_extra: int) -> np.ndarray:
+    """Positions of the prefix 0..a and of n_extra rollout slots after it.
+
+    pos_seq[L, 3] holds the corpus sequence's (t, h, w) positions (None: the
+    index on every axis).  Rollout slot s continues the anchor's position with
+    every axis advancing by s (App. A, "Rollout implementation").
+    """
+    if pos_seq is None:
+        base = np.repeat(np.arange(a + 1, dtype=np.int64)[:, None], 3, axis=1)
+    else:
+        base = np.asarray(pos_seq, dtype=np.int64)[: a + 1]
+    ext = base[a][None, :] + np.arange(1, n_extra + 1, dtype=np.int64)[:, None]
+    return np.concatenate([base, ext], 0)
 
 
 def head_logits(P: Params, hf: np.ndarray) -> np.ndarray:
@@ -239,14 +280,16 @@ def _feats_at(outs: List[np.ndarray], feat_layers: Sequence[int], rows) -> np.nd
 
 
 def prefill_outputs(P: Params, shape, tokens: np.ndarray, given_rows=None, given_mask=None,
-                    emulate_bf16: bool = False):
+                    emulate_bf16: bool = False, positions=None):
     """Teacher-forced forward of one whole corpus sequence.
 
+    positions[T, 3] (optional): (t, h, w) positions; default the index.
     Returns (features [T, n_feat, d], logits [T, V]) at every position.
     """
     T = len(tokens)
     x0 = embed_rows(P, tokens, given_rows, given_mask)
-    outs, hf = decoder_forward(P, shape, x0, np.arange(T), emulate_bf16)
+    pos = np.arange(T) if positions is None else np.asarray(positions)
+    outs, hf = decoder_forward(P, shape, x0, pos, emulate_bf16)
     return _feats_at(outs, shape.feat_layers, slice(None)), head_logits(P, hf)
 
 
@@ -261,13 +304,14 @@ def _prefix_rows(P, tokens_seq, a, given_rows, given_mask):
 
 def rollout_naive(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, block: int,
                   forced: Optional[np.ndarray] = None, given_rows=None, given_mask=None,
-                  emulate_bf16: bool = False):
+                  emulate_bf16: bool = False, positions=None):
     """The definition: for every anchor and slot, a full causal forward with no reuse.
 
     tokens[n_seq, L]; given_rows/given_mask are per-sequence lists (or arrays
     [n_seq, L, d] / [n_seq, L]) of input rows that replace token embeddings.
     forced[n_anchor, block]: where >= 0, the token fed to the next slot
-    instead of the greedy one.
+    instead of the greedy one.  positions[n_seq, L, 3] (optional): (t, h, w)
+    positions of the corpus sequences (M-RoPE); default the index.
     Returns tokens_out int64 [n,B], logprobs [n,B,V], feats [n,B,n_feat,d].
     """
     n = len(anchor_seq)
@@ -283,7 +327,9 @@ def rollout_naive(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, 
         fed: List[int] = []
         for s in range(block):
             rows = prefix if not fed else np.concatenate([prefix, embed_rows(P, fed)], 0)
-            outs, hf = decoder_forward(P, shape, rows, np.arange(a + 1 + len(fed)), emulate_bf16)
+            pos_seq = None if positions is None else positions[sq]
+            outs, hf = decoder_forward(P, shape, rows, slot_positions(pos_seq, a, len(fed)),
+                                       emulate_bf16)
             z = head_logits(P, hf[-1:])[0]
             lp_out[i, s] = log_softmax(z)
             tok_out[i, s] = int(greedy_argmax(z))
@@ -298,7 +344,8 @@ def rollout_naive(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, 
 
 def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos,
                            block: int, feed: np.ndarray, given_rows=None, given_mask=None,
-                           emulate_bf16: bool = False, want_logprobs: bool = True):
+                           emulate_bf16: bool = False, want_logprobs: bool = True,
+                           positions=None):
     """One causal forward per anchor over x_{<=a} . feed[i, :B-1], read at positions a..a+B-1.
 
     feed[n, B] holds the token fed *after* each slot (column B-1 is unused), i.e.
@@ -318,7 +365,9 @@ def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anc
         prefix = _prefix_rows(P, tokens[sq], a, gr, gm)
         fed = [int(t) for t in feed[i, : block - 1]]
         rows = np.concatenate([prefix, embed_rows(P, fed)], 0) if fed else prefix
-        outs, hf = decoder_forward(P, shape, rows, np.arange(a + block), emulate_bf16)
+        pos_seq = None if positions is None else positions[sq]
+        outs, hf = decoder_forward(P, shape, rows, slot_positions(pos_seq, a, len(fed)),
+                                   emulate_bf16)
         z = head_logits(P, hf[a:a + block])
         lp = log_softmax(z)
         if want_logprobs:
@@ -332,7 +381,8 @@ def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anc
 
 
 def rollout_kv_shared(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, block: int,
-                      forced: Optional[np.ndarray] = None, given_rows=None, given_mask=None):
+                      forced: Optional[np.ndarray] = None, given_rows=None, given_mask=None,
+                      positions=None):
     """All anchors batched per step over a shared corpus key/value cache (fp64, no rounding).
 
     Step 0 reads the teacher-forced forward of each corpus sequence at the
@@ -356,12 +406,14 @@ def rollout_kv_shared(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_p
         gr = None if given_rows is None else given_rows[sq]
         gm = None if given_mask is None else given_mask[sq]
         h = embed_rows(P, tokens[sq], gr, gm)
-        pos = np.arange(T)
+        pos = np.arange(T) if positions is None else np.asarray(positions[sq])
         Ks, Vs, outs = [], [], []
         for layer in range(L):
             n1 = rmsnorm(h, P.get("attn_norm", layer), eps)
-            q = rope((n1 @ P.get("wq", layer).T).reshape(T, H, hd), pos, shape.rope_base)
-            k = rope((n1 @ P.get("wk", layer).T).reshape(T, G, hd), pos, shape.rope_base)
+            q = rope((n1 @ P.get("wq", layer).T).reshape(T, H, hd), pos, shape.rope_base,
+                     _sections(shape))
+            k = rope((n1 @ P.get("wk", layer).T).reshape(T, G, hd), pos, shape.rope_base,
+                     _sections(shape))
             v = (n1 @ P.get("wv", layer).T).reshape(T, G, hd)
             Ks.append(k)
             Vs.append(v)
@@ -393,12 +445,18 @@ def rollout_kv_shared(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_p
         nxt = np.where(forced[:, 0] >= 0, forced[:, 0], nxt)
     for s in range(1, block):
         h = embed_rows(P, nxt)  # [n, d]
-        pos = a + s
+        if positions is None:
+            pos = a + s
+        else:  # every axis of the anchor's position advances by s
+            pos = np.stack([np.asarray(positions[int(anchor_seq[i])])[a[i]] + s
+                            for i in range(n)])
         outs = []
         for layer in range(L):
             n1 = rmsnorm(h, P.get("attn_norm", layer), eps)
-            q = rope((n1 @ P.get("wq", layer).T).reshape(n, H, hd), pos, shape.rope_base)
-            k = rope((n1 @ P.get("wk", layer).T).reshape(n, G, hd), pos, shape.rope_base)
+            q = rope((n1 @ P.get("wq", layer).T).reshape(n, H, hd), pos, shape.rope_base,
+                     _sections(shape))
+            k = rope((n1 @ P.get("wk", layer).T).reshape(n, G, hd), pos, shape.rope_base,
+                     _sections(shape))
             v = (n1 @ P.get("wv", layer).T).reshape(n, G, hd)
             o = np.zeros((n, H, hd), P.dt)
             for i in range(n):

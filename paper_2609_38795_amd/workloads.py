@@ -50,6 +50,9 @@ class ModelShape:
     rope_base: float
     dtype: str  # "f32" or "bf16": storage type of weights and GEMM operands
     feat_layers: Tuple[int, ...]  # 0-based decoder layers whose outputs are features
+    # multimodal RoPE: numbers of frequencies driven by the t, h and w position axes
+    # (sum = head_dim / 2); all zero = one position axis (plain RoPE)
+    mrope_sections: Tuple[int, int, int] = (0, 0, 0)
 
     @property
     def q_dim(self) -> int:
@@ -327,6 +330,21 @@ def make_image_rows(w: Workload) -> Tuple[Optional[np.ndarray], Optional[np.ndar
     if w.shape.dtype == "bf16":
         rows = f32_to_bf16_bits(rows)
     return rows, mask.reshape(-1)
+
+
+def grid_positions(seq_len: int, image_side: int) -> np.ndarray:
+    """(t, h, w) positions [seq_len, 3] of a sequence that starts with a square image of
+    image_side x image_side rows, Qwen2-VL style: image row r, column c at (0, r, c); the
+    text that follows starts one past the largest image position and advances all three
+    axes together."""
+    pos = np.zeros((seq_len, 3), np.int32)
+    n_img = image_side * image_side
+    r = np.arange(n_img)
+    pos[:n_img, 1] = r // image_side
+    pos[:n_img, 2] = r % image_side
+    text = image_side + np.arange(seq_len - n_img, dtype=np.int32)
+    pos[n_img:] = text[:, None]
+    return pos
 
 
 @dataclasses.dataclass

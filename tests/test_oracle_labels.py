@@ -198,3 +198,98 @@ def test_ira_supervises_k_minus_j_slots_and_integer_labels():
         assert t0[q] == tokens[q, j - 1]
         np.testing.assert_array_equal(li[q, :B - j], ids[q, j:])
         assert (li[q, B - j:] == -1).all()
+
+
+# ---------------------------------------------------------------- multimodal RoPE
+def test_mrope_with_equal_axes_is_plain_rope():
+    rng = np.random.default_rng(31)
+    x = rng.standard_normal((9, 3, 16))
+    p = rng.integers(0, 500, size=9)
+    plain = O.rope(x, p, 10000.0)
+    for sec in [(2, 3, 3), (8, 0, 0), (0, 4, 4)]:
+        np.testing.assert_allclose(O.rope(x, np.stack([p, p, p], 1), 10000.0, sec), plain,
+                                   rtol=0, atol=1e-13)
+
+
+def test_mrope_sections_select_axes_hand_case():
+    # head_dim 8: frequencies 0..3, theta_i = base^(-2i/8); sections (1, 1, 2):
+    # frequency 0 follows t, 1 follows h, 2 and 3 follow w
+    base = 16.0
+    theta = [base ** (-2 * i / 8) for i in range(4)]
+    pos = np.array([[3, 5, 7]])
+    for i, axis in enumerate([0, 1, 1 + 1, 2]):
+        x = np.zeros((1, 1, 8))
+        x[0, 0, i], x[0, 0, i + 4] = 1.0, 0.5  # the pair (i, i+4)
+        y = O.rope(x, pos, base, (1, 1, 2))
+        ang = pos[0, axis] * theta[i]
+        np.testing.assert_allclose(y[0, 0, i], math.cos(ang) - 0.5 * math.sin(ang), atol=1e-14)
+        np.testing.assert_allclose(y[0, 0, i + 4], 0.5 * math.cos(ang) + math.sin(ang), atol=1e-14)
+        others = [j for j in range(8) if j not in (i, i + 4)]
+        assert np.abs(y[0, 0, others]).max() == 0.0
+
+
+def test_mrope_scores_depend_on_per_axis_offsets_only():
+    rng = np.random.default_rng(5)
+    q, k = rng.standard_normal((1, 1, 16)), rng.standard_normal((1, 1, 16))
+    sec = (2, 3, 3)
+    P, Pk = np.array([[4, 9, 1]]), np.array([[2, 3, 8]])
+    ref = float(np.sum(O.rope(q, P, 1e4, sec) * O.rope(k, Pk, 1e4, sec)))
+    for shift in ([10, 0, 0], [0, 7, 0], [3, 2, 11]):
+        sh = np.array([shift])
+        got = float(np.sum(O.rope(q, P + sh, 1e4, sec) * O.rope(k, Pk + sh, 1e4, sec)))
+        assert abs(got - ref) < 1e-12
+    # a shift of one axis alone does change the score
+    got = float(np.sum(O.rope(q, P + np.array([[0, 5, 0]]), 1e4, sec) * O.rope(k, Pk, 1e4, sec)))
+    assert abs(got - ref) > 1e-6
+
+
+def test_mrope_rollout_forms_agree_and_continue_positions():
+    """Image-grid positions, text after it: naive = teacher-forced = KV-shared, slot 0 = prefill,
+    and forced corpus tokens make slot s equal the prefill output at a+s (all axes advance)."""
+    shape = _tiny_shape(head_dim=8, n_heads=2, n_kv_heads=1, d_model=16, mrope_sections=(1, 1, 2))
+    P = O.Params(W.random_weights(shape, 13, norm_gain="random", scale=0.4))
+    L, side = 30, 3
+    pos = W.grid_positions(L, side)[None]
+    toks = W.random_tokens(shape.vocab, (1, L), 4)
+    a_seq, a_pos = np.zeros(3, np.int32), np.array([9, 15, 22], np.int32)
+    tk, lp, ft = O.rollout_naive(P, shape, toks, a_seq, a_pos, 4, positions=pos)
+    tk2, lp2, ft2, _ = O.rollout_teacher_forced(P, shape, toks, a_seq, a_pos, 4, tk, positions=pos)
+    tk3, lp3, ft3 = O.rollout_kv_shared(P, shape, toks, a_seq, a_pos, 4, positions=pos)
+    np.testing.assert_array_equal(tk, tk2)
+    np.testing.assert_array_equal(tk, tk3)
+    np.testing.assert_allclose(lp, lp2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lp, lp3, rtol=0, atol=1e-12)
+    feats, z = O.prefill_outputs(P, shape, toks[0], positions=pos[0])
+    forced = np.stack([toks[0, a + 1:a + 5] for a in a_pos]).astype(np.int64)
+    tkf, lpf, ftf = O.rollout_naive(P, shape, toks, a_seq, a_pos, 4, forced=forced, positions=pos)
+    for i, a in enumerate(a_pos):
+        for s in range(4):
+            np.testing.assert_allclose(lpf[i, s], O.log_softmax(z[a + s]), rtol=0, atol=1e-12)
+    # the grid positions matter: with index positions the outputs differ
+    tk4, lp4, _ = O.rollout_naive(P, shape, toks, a_seq, a_pos, 4)
+    assert np.abs(lp4 - lp).max() > 1e-6
+
+
+# ---------------------------------------------------------------- early end (EOS)
+def test_active_slots_and_weights_hand_case():
+    toks = np.array([[5, 9, 2, 9], [1, 2, 3, 4], [9, 9, 9, 9]])
+    act = LB.active_slots(toks, 9)
+    np.testing.assert_array_equal(act, [[1, 1, 0, 0], [1, 1, 1, 1], [1, 0, 0, 0]])
+    w = LB.slot_weights(toks, 9, gamma=2.0)
+    env = LB.slot_envelope(4)
+    np.testing.assert_allclose(w[0], [env[0], env[1], 0, 0])
+    np.testing.assert_allclose(w[1], env)
+    np.testing.assert_allclose(LB.slot_weights(toks, None), np.tile(env, (3, 1)))
+
+
+def test_ira_weights_stop_at_primary_end():
+    B = 8
+    toks = np.array([[3, 4, 5, 7, 1, 1, 1, 1]])  # EOS = 7 fed after index 3
+    lab = np.zeros((1, B))
+    _, _, w, _ = LB.ira_secondary(toks, lab, [0], [2], eos_id=7)
+    # the EOS is produced at primary index 3 (fed before index 4): indices 0..3 are active.
+    # j = 2: index s' inherits primary index 2 + s' -> s' = 0, 1 active
+    env = LB.slot_envelope(B)
+    np.testing.assert_allclose(w[0], [env[0], env[1], 0, 0, 0, 0, 0, 0])
+    _, _, w2, _ = LB.ira_secondary(toks, lab, [0], [2])
+    assert (w2[0] > 0).sum() == (B - 1) - 2
