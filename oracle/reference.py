@@ -170,11 +170,15 @@ def rope(x: np.ndarray, positions: np.ndarray, base: float, sections=None) -> np
     return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
 
 
-def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                         round_probs=None) -> np.ndarray:
     """Causal softmax attention. q[T,H,hd], k/v[T,G,hd] -> out[T,H,hd].
 
     Query head j reads key/value head j // (H/G); scores are scaled by
-    1/sqrt(hd); position t sees keys 0..t.
+    1/sqrt(hd); position t sees keys 0..t.  round_probs (optional): a rounding
+    applied to the unnormalised probabilities exp(s - max) where they multiply
+    the values, the normaliser staying in working precision (how a bf16
+    matrix-core attention evaluates the value product).
     """
     T, H, hd = q.shape
     G = k.shape[1]
@@ -188,8 +192,11 @@ def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndar
         s[mask] = -np.inf
         s = s - s.max(axis=1, keepdims=True)
         p = np.exp(s)
-        p /= p.sum(axis=1, keepdims=True)
-        out[:, j, :] = p @ v[:, g, :]
+        if round_probs is None:
+            p /= p.sum(axis=1, keepdims=True)
+            out[:, j, :] = p @ v[:, g, :]
+        else:
+            out[:, j, :] = (round_probs(p) @ v[:, g, :]) / p.sum(axis=1, keepdims=True)
     return out
 
 
@@ -219,9 +226,15 @@ def embed_rows(P: Params, tokens: Sequence[int], given_rows: Optional[np.ndarray
 
 
 def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
-                    emulate_bf16: bool = False, want_layers: bool = True):
-    """Full causal forward.  Returns (outputs of every layer [L][T,d], final-normed [T,d])."""
+                    emulate_bf16: bool = False, want_layers: bool = True,
+                    bf16_probs: bool = False):
+    """Full causal forward.  Returns (outputs of every layer [L][T,d], final-normed [T,d]).
+
+    bf16_probs: with emulate_bf16, attention also rounds its unnormalised
+    probabilities to bf16 before the value product (a second valid bf16
+    evaluation, used to size the bf16 noise floor)."""
     rnd = bf16_round if emulate_bf16 else _ident
+    rp = bf16_round if (emulate_bf16 and bf16_probs) else None
     dt = P.dt
     H, G, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     eps = shape.rms_eps
@@ -236,7 +249,7 @@ def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
         q = rnd(rope(q, positions, shape.rope_base, _sections(shape)))
         k = rnd(rope(k, positions, shape.rope_base, _sections(shape)))
         v = rnd(v)
-        o = rnd(causal_gqa_attention(q, k, v).reshape(T, H * hd))
+        o = rnd(causal_gqa_attention(q, k, v, rp).reshape(T, H * hd))
         h = h + o @ P.get("wo", layer).T
         n2 = rnd(rmsnorm(h, P.get("ffn_norm", layer), eps))
         act = rnd(silu(n2 @ P.get("w_gate", layer).T) * (n2 @ P.get("w_up", layer).T))
@@ -345,12 +358,13 @@ def rollout_naive(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, 
 def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos,
                            block: int, feed: np.ndarray, given_rows=None, given_mask=None,
                            emulate_bf16: bool = False, want_logprobs: bool = True,
-                           positions=None):
+                           positions=None, bf16_probs: bool = False):
     """One causal forward per anchor over x_{<=a} . feed[i, :B-1], read at positions a..a+B-1.
 
     feed[n, B] holds the token fed *after* each slot (column B-1 is unused), i.e.
     the input of slot s+1 is feed[i, s].  Returns (argmax tokens [n,B],
     logprobs [n,B,V] or None, feats [n,B,n_feat,d], top-2 margins [n,B]).
+    bf16_probs: see :func:`decoder_forward`.
     """
     n = len(anchor_seq)
     V, d, nf = shape.vocab, shape.d_model, len(shape.feat_layers)
@@ -367,7 +381,7 @@ def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anc
         rows = np.concatenate([prefix, embed_rows(P, fed)], 0) if fed else prefix
         pos_seq = None if positions is None else positions[sq]
         outs, hf = decoder_forward(P, shape, rows, slot_positions(pos_seq, a, len(fed)),
-                                   emulate_bf16)
+                                   emulate_bf16, bf16_probs=bf16_probs)
         z = head_logits(P, hf[a:a + block])
         lp = log_softmax(z)
         if want_logprobs:

@@ -13,9 +13,12 @@ Parity rules (fp32 / bf16):
 * features: max-abs difference, divided by the RMS of the oracle's feature row
   for bf16, <= ``ft_tol``.
 
-The bf16 noise floor is the difference between two valid bf16 evaluations of
-the same model that round at the same points but accumulate in different
-precisions (oracle with fp64 vs fp32 working precision).
+The bf16 noise floor is the largest difference between the fp64 bf16 evaluation
+and another valid bf16 evaluation of the same model: one that rounds at the
+same points but accumulates in fp32, and one whose attention also rounds its
+unnormalised probabilities to bf16 before the value product, as a bf16
+matrix-core attention must (the method fixes bf16 arithmetic, not where
+attention rounds).
 """
 from __future__ import annotations
 
@@ -55,16 +58,21 @@ def _given(inp, sel_seq):
     return rows, mask
 
 
-def oracle_rollout(inp, shape, anchor_seq, anchor_pos, block, feed, emulate, dt=np.float64):
+def oracle_rollout(inp, shape, anchor_seq, anchor_pos, block, feed, emulate, dt=np.float64,
+                   positions=None, bf16_probs=False):
     """Teacher-forced oracle along ``feed`` (tokens fed after each slot)."""
     P = O.Params(inp.weights, dt=dt, cache=shape.n_params() < 400_000_000)
     rows, mask = _given(inp, anchor_seq)
     return O.rollout_teacher_forced(P, shape, inp.tokens, anchor_seq, anchor_pos, block, feed,
-                                    given_rows=rows, given_mask=mask, emulate_bf16=emulate)
+                                    given_rows=rows, given_mask=mask, emulate_bf16=emulate,
+                                    positions=positions, bf16_probs=bf16_probs)
 
 
-def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = None) -> Report:
+def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = None,
+            positions=None) -> Report:
     """Compare the GPU rollout of anchors ``sel`` (indices into the workload's anchors).
+
+    positions[n_seq, L, 3] (optional): the (t, h, w) positions given to the prefill.
 
     gpu_run(forced or None) -> (tokens [n,B], logprobs [n,B,V], feats [n,B,nf,d]) as numpy,
     for exactly the selected anchors.
@@ -74,14 +82,19 @@ def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = Non
     a_pos = inp.anchor_pos[sel]
     g_tok, g_lp, g_ft = gpu_run(None)
     # oracle along the GPU's own path: equals the naive definition wherever they agree
-    o_tok, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, bf16)
+    o_tok, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, bf16,
+                                              positions=positions)
     floor_lp = floor_ft = 0.0
     if bf16 and (measure_floor is None or measure_floor):
         e_tok, e_lp, e_ft, _ = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, True,
-                                              dt=np.float32)
-        floor_lp = float(np.abs(e_lp - o_lp).max())
-        rms = np.sqrt(np.mean(o_ft ** 2, axis=-1, keepdims=True)) if o_ft.size else 1.0
-        floor_ft = float((np.abs(e_ft - o_ft) / rms).max()) if o_ft.size else 0.0
+                                              dt=np.float32, positions=positions)
+        p_tok, p_lp, p_ft, _ = oracle_rollout(inp, shape, a_seq, a_pos, block, g_tok, True,
+                                              positions=positions, bf16_probs=True)
+        floor_lp = float(max(np.abs(e_lp - o_lp).max(), np.abs(p_lp - o_lp).max()))
+        if o_ft.size:
+            rms = np.sqrt(np.mean(o_ft ** 2, axis=-1, keepdims=True))
+            floor_ft = float(max((np.abs(e_ft - o_ft) / rms).max(),
+                                 (np.abs(p_ft - o_ft) / rms).max()))
     if bf16:
         tok_margin = max(1e-2, 2 * floor_lp)
         lp_tol = max(2e-2, 2 * floor_lp)
@@ -104,7 +117,8 @@ def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = Non
         # continue on the oracle's path: feed the oracle's own tokens to both sides
         forced = o_tok.astype(np.int32).copy()
         g_tok, g_lp, g_ft = gpu_run(forced)
-        o_tok2, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, forced, bf16)
+        o_tok2, o_lp, o_ft, margin = oracle_rollout(inp, shape, a_seq, a_pos, block, forced, bf16,
+                                                    positions=positions)
         conf = margin > tok_margin
         confident_bad += int(((g_tok != o_tok2) & conf).sum())
         forced_rerun = True

@@ -152,6 +152,26 @@ def test_attention_hand_case_scale_and_mask():
                                rtol=1e-14)
 
 
+def test_attention_rounded_probabilities_hand_case():
+    """round_probs rounds exp(s - max) where it weights the values; the normaliser keeps
+    the exact sum.  Position 1: scores [1, 0] -> p = [1, e^-1]; bf16(e^-1) = 188/512."""
+    q = np.zeros((2, 1, 4)); k = np.zeros((2, 1, 4)); v = np.zeros((2, 1, 4))
+    q[1, 0, 0] = 2.0; k[0, 0, 0] = 1.0
+    v[0, 0] = [1, 2, 3, 4]; v[1, 0] = [5, 6, 7, 8]
+    out = O.causal_gqa_attention(q, k, v, round_probs=O.bf16_round)
+    e1 = math.exp(-1.0)
+    want = (np.array([1, 2, 3, 4]) + (188 / 512) * np.array([5, 6, 7, 8])) / (1 + e1)
+    np.testing.assert_allclose(out[1, 0], want, rtol=1e-14)
+    np.testing.assert_allclose(out[0, 0], [1, 2, 3, 4], rtol=1e-15)
+    # probabilities that bf16 holds exactly (equal scores: all ones) are unchanged
+    rng = np.random.default_rng(5)
+    vv = rng.standard_normal((7, 2, 5))
+    kk = rng.standard_normal((7, 2, 5))
+    np.testing.assert_allclose(
+        O.causal_gqa_attention(np.zeros((7, 4, 5)), kk, vv, round_probs=O.bf16_round),
+        O.causal_gqa_attention(np.zeros((7, 4, 5)), kk, vv), rtol=1e-14, atol=1e-15)
+
+
 def test_attention_uniform_is_running_mean():
     rng = np.random.default_rng(4)
     v = rng.standard_normal((9, 2, 5))
