@@ -77,7 +77,13 @@ typedef enum { ALR_F32 = 0, ALR_BF16 = 1 } alr_dtype;
  *   multiples of 64; head_dim is even and <= 256; n_heads % n_kv_heads == 0;
  *   (n_heads*head_dim/2) and (n_kv_heads*head_dim/2) are multiples of 32;
  *   vocab is a multiple of 64; 0 <= feat_layers[i] < n_layers;
- *   max_pos >= 1 bounds every position a slot may reach (a + block - 1). */
+ *   max_pos >= 1 bounds every position a slot may reach (a + block - 1), on
+ *   every position axis.
+ *   mrope_sections: multimodal RoPE (App. A, "Rollout implementation": the
+ *   three M-RoPE axes advance together).  The head_dim/2 rotary frequencies
+ *   are split into consecutive runs of mrope_sections[0], [1], [2] driven by the
+ *   t, h and w positions of a token; all zero = plain RoPE on one position
+ *   axis.  Otherwise each >= 0 and their sum == head_dim / 2. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
   float rms_eps, rope_base;
@@ -85,6 +91,7 @@ typedef struct {
   int32_t max_pos;
   int32_t n_feat;  /* 0 .. ALR_MAX_FEAT */
   int32_t feat_layers[ALR_MAX_FEAT];
+  int32_t mrope_sections[3];
 } alr_config;
 
 /* Device pointers to the weights, element type given by alr_config.dtype
@@ -155,6 +162,19 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
 alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len,
                        const int32_t* tokens, const void* embeds,
                        const uint8_t* embed_mask, float* feats_out, alr_stream stream);
+
+/* alr_prefill with explicit token positions (RoPE / M-RoPE).
+ *   positions  HOST int32 [sum seq_len][3]: (t, h, w) position of every corpus
+ *              token, each in [0, max_pos); or NULL for the token's index in its
+ *              sequence on every axis (then identical to alr_prefill).  With
+ *              plain RoPE (mrope_sections all zero) only the t column is used.
+ * A rollout slot s of an anchor sits at the anchor token's position plus s on
+ * every axis, so each axis value + block - 1 must stay below max_pos (checked
+ * by the rollout calls).  Other arguments and checks as in alr_prefill. */
+alr_status alr_prefill_positions(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len,
+                                 const int32_t* tokens, const int32_t* positions,
+                                 const void* embeds, const uint8_t* embed_mask, float* feats_out,
+                                 alr_stream stream);
 
 /* Greedy rollout of `block` slots from every anchor of the last prefill.
  *   anchor_seq, anchor_pos  HOST int32 [n_anchor]: sequence index and position;
@@ -245,14 +265,25 @@ alr_status alr_corpus_labels(alr_ctx* ctx, int32_t n_anchor, const int32_t* anch
  *               index j + s' (paper slot j + k with k = s'+1) while j + s' <=
  *               block-1, else ids -1, log-probs -inf, tail 0.
  *   weight_out  DEVICE fp32 [n_secondary, block]: w_k = exp(-(k-1)/gamma)
- *               where j + k <= block-1, else 0 (unsupervised tail).
+ *               where j + k <= block-1 and the primary had not ended before
+ *               the inherited slot (no eos_id among tokens[p, 0 .. j+s'-1];
+ *               eos_id < 0: no early end), else 0 (unsupervised tail).
  * gamma > 0.  n_secondary = 0 is a no-op. */
 alr_status alr_ira_assemble(alr_ctx* ctx, int32_t n_primary, int32_t block,
                             const int32_t* tokens, const int32_t* top_ids, const float* top_logp,
                             const float* tail, int32_t n_secondary, const int32_t* sec_primary,
-                            const int32_t* sec_offset, float gamma, int32_t* token0_out,
-                            int32_t* top_ids_out, float* top_logp_out, float* tail_out,
-                            float* weight_out, alr_stream stream);
+                            const int32_t* sec_offset, float gamma, int32_t eos_id,
+                            int32_t* token0_out, int32_t* top_ids_out, float* top_logp_out,
+                            float* tail_out, float* weight_out, alr_stream stream);
+
+/* Slot weights of ALR blocks (Eq. 1 envelope; Sec. 3.2: slots that follow an
+ * early end of the rollout are masked): weight_out[i, s] = exp(-s / gamma)
+ * while no token equal to eos_id occurs in tokens[i, 0 .. s-1] (the tokens fed
+ * before index s), else 0.  eos_id < 0: no early end.  tokens DEVICE int32
+ * [n, block] (e.g. alr_rollout's tokens_out), weight_out DEVICE fp32 [n, block];
+ * n >= 0, block >= 1, gamma > 0. */
+alr_status alr_slot_weights(alr_ctx* ctx, int32_t n, int32_t block, const int32_t* tokens,
+                            int32_t eos_id, float gamma, float* weight_out, alr_stream stream);
 
 /* Message of the last failing call on ctx ("" if none); ctx may be NULL, then
  * the message of the last failing alr_create in this thread is returned. */

@@ -23,8 +23,8 @@ STATUS = {0: "ALR_OK", 1: "ALR_E_INVALID_ARG", 2: "ALR_E_OUT_OF_RANGE", 3: "ALR_
 
 # Every function the C headers declare (include/alr.h, include/alr_debug.h).
 EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_create",
-           "alr_prefill", "alr_rollout", "alr_rollout_topk", "alr_corpus_labels",
-           "alr_ira_assemble", "alr_last_error", "alr_status_string", "alr_destroy",
+           "alr_prefill", "alr_prefill_positions", "alr_rollout", "alr_rollout_topk",
+           "alr_corpus_labels", "alr_ira_assemble", "alr_slot_weights", "alr_last_error", "alr_status_string", "alr_destroy",
            "alr_debug_gemm", "alr_profile_start", "alr_profile_stop")
 ALR_TOPK = 8
 
@@ -36,7 +36,8 @@ class AlrConfig(ctypes.Structure):
                 ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32),
                 ("max_pos", ctypes.c_int32), ("n_feat", ctypes.c_int32),
-                ("feat_layers", ctypes.c_int32 * ALR_MAX_FEAT)]
+                ("feat_layers", ctypes.c_int32 * ALR_MAX_FEAT),
+                ("mrope_sections", ctypes.c_int32 * 3)]
 
 
 class AlrLimits(ctypes.Structure):
@@ -87,6 +88,10 @@ def load_library() -> ctypes.CDLL:
     lib.alr_create.restype = ctypes.c_int
     lib.alr_prefill.argtypes = [vp, i32, i32p, vp, vp, vp, vp, vp]
     lib.alr_prefill.restype = ctypes.c_int
+    lib.alr_prefill_positions.argtypes = [vp, i32, i32p, vp, i32p, vp, vp, vp, vp]
+    lib.alr_prefill_positions.restype = ctypes.c_int
+    lib.alr_slot_weights.argtypes = [vp, i32, i32, vp, i32, ctypes.c_float, vp, vp]
+    lib.alr_slot_weights.restype = ctypes.c_int
     lib.alr_rollout.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp]
     lib.alr_rollout.restype = ctypes.c_int
     lib.alr_rollout_topk.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -95,7 +100,7 @@ def load_library() -> ctypes.CDLL:
                                       vp]
     lib.alr_corpus_labels.restype = ctypes.c_int
     lib.alr_ira_assemble.argtypes = [vp, i32, i32, vp, vp, vp, vp, i32, i32p, i32p,
-                                     ctypes.c_float, vp, vp, vp, vp, vp, vp]
+                                     ctypes.c_float, i32, vp, vp, vp, vp, vp, vp]
     lib.alr_ira_assemble.restype = ctypes.c_int
     lib.alr_last_error.argtypes = [vp]
     lib.alr_last_error.restype = ctypes.c_char_p
@@ -124,6 +129,8 @@ def make_config(shape, max_pos: int) -> AlrConfig:
     c.n_feat = len(shape.feat_layers)
     for i, f in enumerate(shape.feat_layers):
         c.feat_layers[i] = f
+    for i, v in enumerate(getattr(shape, "mrope_sections", (0, 0, 0))):
+        c.mrope_sections[i] = v
     return c
 
 
@@ -230,14 +237,17 @@ class Engine:
 
     # ---------------------------------------------------------------- calls
     def prefill(self, tokens, seq_len: Sequence[int], embeds=None, embed_mask=None,
-                feats_out=None):
-        """tokens: device int32 tensor [sum seq_len]; embeds/embed_mask device tensors or None."""
+                feats_out=None, positions=None):
+        """tokens: device int32 tensor [sum seq_len]; embeds/embed_mask device tensors or None;
+        positions: host int array [sum seq_len, 3] of (t, h, w) positions, or None."""
         sl = np.ascontiguousarray(seq_len, dtype=np.int32)
         self._seq_len = sl
-        st = self.lib.alr_prefill(self.ctx, len(sl), _i32p(sl), tokens.data_ptr(),
-                                  None if embeds is None else embeds.data_ptr(),
-                                  None if embed_mask is None else embed_mask.data_ptr(),
-                                  None if feats_out is None else feats_out.data_ptr(), self._sp())
+        pos = None if positions is None else np.ascontiguousarray(positions, dtype=np.int32)
+        st = self.lib.alr_prefill_positions(
+            self.ctx, len(sl), _i32p(sl), tokens.data_ptr(), None if pos is None else _i32p(pos),
+            None if embeds is None else embeds.data_ptr(),
+            None if embed_mask is None else embed_mask.data_ptr(),
+            None if feats_out is None else feats_out.data_ptr(), self._sp())
         if st != 0:
             self._err(st)
 
@@ -327,7 +337,7 @@ class Engine:
         return r
 
     def ira_assemble(self, tokens, top_ids, top_logp, tail, sec_primary, sec_offset,
-                     gamma: float = 2.0):
+                     gamma: float = 2.0, eos_id: int = -1):
         """Secondary blocks from primary rollout labels -> (token0, top_ids, top_logp, tail,
         weight) device tensors."""
         torch = self.torch
@@ -340,12 +350,23 @@ class Engine:
         w = torch.empty((q, block), dtype=torch.float32, device=self.device)
         st = self.lib.alr_ira_assemble(self.ctx, n_prim, block, tokens.data_ptr(),
                                        top_ids.data_ptr(), top_logp.data_ptr(), tail.data_ptr(),
-                                       q, _i32p(sp), _i32p(so), gamma, t0.data_ptr(),
+                                       q, _i32p(sp), _i32p(so), gamma, eos_id, t0.data_ptr(),
                                        ti.data_ptr(), tl.data_ptr(), tt.data_ptr(), w.data_ptr(),
                                        self._sp())
         if st != 0:
             self._err(st)
         return t0, ti, tl, tt, w
+
+    def slot_weights(self, tokens, eos_id: int = -1, gamma: float = 2.0):
+        """ALR slot weights [n, block] from rollout tokens (device int32 [n, block])."""
+        torch = self.torch
+        n, block = tokens.shape
+        w = torch.empty((n, block), dtype=torch.float32, device=self.device)
+        st = self.lib.alr_slot_weights(self.ctx, n, block, tokens.data_ptr(), eos_id, gamma,
+                                       w.data_ptr(), self._sp())
+        if st != 0:
+            self._err(st)
+        return w
 
 
 PROF_SITES = {"prefill_qkv": 1, "prefill_attn": 2, "prefill_o": 3, "prefill_gu": 4,

@@ -33,8 +33,9 @@ struct EpiQKV {
   long vt_stride;
   const float* cosT;  // [max_pos, hd/2]
   const float* sinT;
-  const int* pos;     // position of row r is pos[r] + pos_add
+  const int* pos;     // (t, h, w) position of row r: pos[3 r + axis] + pos_add
   int pos_add;
+  int sec0, sec01;    // frequencies < sec0 follow axis t, < sec01 axis h, the rest axis w
   int H, G, hd;
   __device__ __forceinline__ void operator()(int row, int c, float lo, float hi) const {
     const int half = hd >> 1;
@@ -51,7 +52,8 @@ struct EpiQKV {
       }
       const int f = 32 * (cl >> 6) + (cl & 63);
       const int head = f / half, i = f - head * half;
-      const long p = (long)(pos[row] + pos_add);
+      const int axis = (i < sec0) ? 0 : ((i < sec01) ? 1 : 2);
+      const long p = (long)(pos[3 * row + axis] + pos_add);
       const float cs = cosT[p * half + i], sn = sinT[p * half + i];
       Elt<OutT>::st(dst + head * hd + i, lo * cs - hi * sn);
       Elt<OutT>::st(dst + head * hd + i + half, hi * cs + lo * sn);

@@ -393,11 +393,12 @@ __global__ __launch_bounds__(256) void erase_gates_kernel(const int* __restrict_
 // of primary block p = prim[q] (1 <= j <= block-1).  token0[q] = tokens[p, j-1]
 // (y*_j); its index s' copies the primary's labels at index j + s' while that
 // is <= block-1 (else ids -1, log-probs -inf, tail 0); weight[q, s'] =
-// exp(-s'/gamma) when j + s' + 1 <= block - 1, else 0.  One thread per (q, s').
+// exp(-s'/gamma) when j + s' + 1 <= block - 1 and (eos_id >= 0) the primary
+// fed no EOS before index j + s', else 0.  One thread per (q, s').
 __global__ __launch_bounds__(256) void ira_assemble_kernel(
     const int* __restrict__ prim, const int* __restrict__ off, int n_sec, int block,
     const int* __restrict__ tokens, const int* __restrict__ top_ids,
-    const float* __restrict__ top_logp, const float* __restrict__ tail, float gamma,
+    const float* __restrict__ top_logp, const float* __restrict__ tail, float gamma, int eos_id,
     int* __restrict__ token0, int* __restrict__ s_ids, float* __restrict__ s_logp,
     float* __restrict__ s_tail, float* __restrict__ s_weight) {
   const long t = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -421,7 +422,25 @@ __global__ __launch_bounds__(256) void ira_assemble_kernel(
     }
     s_tail[dst] = 0.f;
   }
-  s_weight[dst] = (j + s2 + 1 <= block - 1) ? expf(-(float)s2 / gamma) : 0.f;
+  bool alive = src <= block - 1;
+  if (eos_id >= 0)  // the primary's slot src is masked once an EOS was fed before it
+    for (int t = 0; t < src && t < block && alive; ++t)
+      alive = tokens[(long)p * block + t] != eos_id;
+  s_weight[dst] = (j + s2 + 1 <= block - 1 && alive) ? expf(-(float)s2 / gamma) : 0.f;
+}
+
+// Slot weights: w[i, s] = exp(-s / gamma) while no EOS occurs in tokens[i, 0 .. s-1],
+// else 0.  One thread per block row.
+__global__ __launch_bounds__(256) void slot_weights_kernel(const int* __restrict__ tokens,
+                                                           int n, int block, int eos_id,
+                                                           float gamma, float* __restrict__ w) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  bool alive = true;
+  for (int s = 0; s < block; ++s) {
+    w[(long)i * block + s] = alive ? expf(-(float)s / gamma) : 0.f;
+    if (eos_id >= 0 && tokens[(long)i * block + s] == eos_id) alive = false;
+  }
 }
 
 // Corpus tokens kept for the corpus labels: ctok[i] = tokens[i], or -1 where

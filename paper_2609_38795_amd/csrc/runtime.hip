@@ -50,7 +50,7 @@ struct Layout {
   size_t kp, vp, kvp_layer_stride;
   size_t feat_store, hf_store;
   size_t resid, xnorm, qbuf, attn, act;
-  size_t i_tokpos, i_rowstart, i_perm, i_apos, i_atok, i_aseq, i_alen, i_cur;
+  size_t i_tokpos, i_rowstart, i_perm, i_apos, i_rpos, i_atok, i_aseq, i_alen, i_cur;
   size_t i_valid, i_target, i_ira, i_ctok, logits;
   size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
@@ -92,6 +92,14 @@ alr_status check_config_impl(const alr_config* c, char* msg, size_t len) {
     return fmt_msg(msg, len,
                    "head_dim must be even and <= 256, and heads*head_dim/2 a multiple of 32"),
            ALR_E_UNSUPPORTED;
+  {
+    const int* ms = c->mrope_sections;
+    const bool none = ms[0] == 0 && ms[1] == 0 && ms[2] == 0;
+    if (!none && (ms[0] < 0 || ms[1] < 0 || ms[2] < 0 || ms[0] + ms[1] + ms[2] != c->head_dim / 2))
+      return fmt_msg(msg, len, "mrope_sections (%d, %d, %d) must be all zero or non-negative with "
+                               "sum head_dim/2 = %d", ms[0], ms[1], ms[2], c->head_dim / 2),
+             ALR_E_INVALID_ARG;
+  }
   if (c->n_feat < 0 || c->n_feat > ALR_MAX_FEAT)
     return fmt_msg(msg, len, "n_feat %d outside [0, %d]", c->n_feat, ALR_MAX_FEAT),
            ALR_E_INVALID_ARG;
@@ -172,10 +180,11 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.qbuf = take(R * qd * es);
   L.attn = take(R * qd * es);
   L.act = take(R * F * es);
-  L.i_tokpos = take(T * 4);
+  L.i_tokpos = take(T * 3 * 4);
   L.i_rowstart = take(T * 4);
   L.i_perm = take(NA * 4);
   L.i_apos = take(NA * 4);
+  L.i_rpos = take(NA * 3 * 4);
   L.i_atok = take(NA * 4);
   L.i_aseq = take(NA * 4);
   L.i_alen = take(NA * 4);
@@ -271,7 +280,7 @@ struct alr_ctx {
   std::vector<int> seq_len, seq_off;
   std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
   std::vector<PrefillItem> h_pwork;
-  std::vector<int> h_anch;  // perm | apos | atok | aseq | alen, each n_anchor long
+  std::vector<int> h_anch;  // perm | apos | atok | aseq | alen (n each) | rope positions (3n)
   std::vector<int> h_ira;   // secondary primaries | offsets
   std::vector<DecodeItem> h_dwork;
   std::vector<DecodeGroup> h_groups;
@@ -479,6 +488,12 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
   eq.H = H;
   eq.G = G;
   eq.hd = hd;
+  {
+    const int* ms = c.mrope_sections;
+    const bool none = ms[0] == 0 && ms[1] == 0 && ms[2] == 0;
+    eq.sec0 = none ? hd / 2 : ms[0];
+    eq.sec01 = none ? hd / 2 : ms[0] + ms[1];
+  }
   eq.vt_col = nullptr;
   eq.vt_stride = 0;
   if (!decode) {
@@ -495,7 +510,7 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
     eq.k = kp + (long)(s - 1) * kvd;
     eq.v = vp + (long)(s - 1) * kvd;
     eq.kv_rs = priv_rs;
-    eq.pos = ctx->at<int>(L.i_apos);
+    eq.pos = ctx->at<int>(L.i_rpos);
     eq.pos_add = s;
   }
   if (decode)
@@ -966,11 +981,27 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
 alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, const int32_t* tokens,
                        const void* embeds, const uint8_t* embed_mask, float* feats_out,
                        alr_stream stream) {
+  return alr_prefill_positions(ctx, n_seq, seq_len, tokens, nullptr, embeds, embed_mask, feats_out,
+                               stream);
+}
+
+alr_status alr_prefill_positions(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len,
+                                 const int32_t* tokens, const int32_t* positions,
+                                 const void* embeds, const uint8_t* embed_mask, float* feats_out,
+                                 alr_stream stream) {
   if (!ctx) return ALR_E_INVALID_ARG;
   char msg[256];
   alr_status st = check_prefill_impl(ctx->cfg, ctx->lim, n_seq, seq_len, tokens, embeds,
                                      embed_mask, msg, sizeof(msg));
   if (st != ALR_OK) return fail(ctx, st, "%s", msg);
+  if (positions) {
+    long tot = 0;
+    for (int i = 0; i < n_seq; ++i) tot += seq_len[i];
+    for (long t = 0; t < 3 * tot; ++t)
+      if (positions[t] < 0 || positions[t] >= ctx->cfg.max_pos)
+        return fail(ctx, ALR_E_OUT_OF_RANGE, "positions[%ld][%ld] = %d outside [0, max_pos=%d)",
+                    t / 3, t % 3, positions[t], ctx->cfg.max_pos);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const alr_config& c = ctx->cfg;
   const int rep = c.n_heads / c.n_kv_heads;
@@ -980,7 +1011,7 @@ alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, cons
   ctx->seq_off.assign(n_seq + 1, 0);
   for (int i = 0; i < n_seq; ++i) ctx->seq_off[i + 1] = ctx->seq_off[i] + seq_len[i];
   const int M = ctx->seq_off[n_seq];
-  ctx->h_tokpos.resize(M);
+  ctx->h_tokpos.resize((size_t)3 * M);
   ctx->h_rowstart.resize(M);
   ctx->h_pwork.clear();
   ctx->h_vtcol.resize(M);
@@ -989,7 +1020,8 @@ alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, cons
   for (int i = 0; i < n_seq; ++i) {
     ctx->seq_vcol[i] = vcol;
     for (int p = 0; p < seq_len[i]; ++p) {
-      ctx->h_tokpos[ctx->seq_off[i] + p] = p;
+      const long row = ctx->seq_off[i] + p;
+      for (int ax = 0; ax < 3; ++ax) ctx->h_tokpos[3 * row + ax] = positions ? positions[3 * row + ax] : p;
       ctx->h_rowstart[ctx->seq_off[i] + p] = ctx->seq_off[i];
       ctx->h_vtcol[ctx->seq_off[i] + p] = vcol + p;
     }
@@ -1007,7 +1039,7 @@ alr_status alr_prefill(alr_ctx* ctx, int32_t n_seq, const int32_t* seq_len, cons
   if (ctx->h_pwork.size() > ctx->L.max_pwork)
     return fail(ctx, ALR_E_WORKSPACE, "prefill work list overflow");
   const Layout& L = ctx->L;
-  st = upload(ctx, ctx->at<int>(L.i_tokpos), ctx->h_tokpos.data(), (size_t)M * 4, s);
+  st = upload(ctx, ctx->at<int>(L.i_tokpos), ctx->h_tokpos.data(), (size_t)M * 3 * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_rowstart), ctx->h_rowstart.data(), (size_t)M * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_vtcol), ctx->h_vtcol.data(), (size_t)M * 4, s);
   if (st == ALR_OK)
@@ -1042,12 +1074,13 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
     if (anchor_pos[x] != anchor_pos[y]) return anchor_pos[x] < anchor_pos[y];
     return x < y;
   });
-  ctx->h_anch.resize((size_t)5 * n);
+  ctx->h_anch.resize((size_t)8 * n);
   int* perm = ctx->h_anch.data();
   int* apos = perm + n;
   int* atok = perm + 2 * n;
   int* aseq = perm + 3 * n;
   int* alen = perm + 4 * n;
+  int* rpos = perm + 5 * n;  // [n][3]: RoPE position of the anchor token on each axis
   for (int r = 0; r < n; ++r) {
     const int i = order[r];
     perm[r] = i;
@@ -1055,6 +1088,13 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
     atok[r] = ctx->seq_off[anchor_seq[i]] + anchor_pos[i];
     aseq[r] = ctx->seq_off[anchor_seq[i]];
     alen[r] = ctx->seq_len[anchor_seq[i]];
+    for (int ax = 0; ax < 3; ++ax) {
+      rpos[3 * r + ax] = ctx->h_tokpos[3 * (size_t)atok[r] + ax];
+      if ((long)rpos[3 * r + ax] + block - 1 >= c.max_pos)
+        return fail(ctx, ALR_E_OUT_OF_RANGE,
+                    "anchor %d: position %d on axis %d + block - 1 >= max_pos %d", i,
+                    rpos[3 * r + ax], ax, c.max_pos);
+    }
   }
   ctx->h_dwork.clear();
   ctx->h_groups.clear();
@@ -1145,6 +1185,7 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_atok), atok, (size_t)n * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_aseq), aseq, (size_t)n * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_alen), alen, (size_t)n * 4, s);
+  if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_rpos), rpos, (size_t)n * 3 * 4, s);
   if (st == ALR_OK && !ctx->h_dwork.empty())
     st = upload(ctx, ctx->at<DecodeItem>(L.i_dwork), ctx->h_dwork.data(),
                 ctx->h_dwork.size() * sizeof(DecodeItem), s);
@@ -1221,9 +1262,9 @@ alr_status alr_corpus_labels(alr_ctx* ctx, int32_t n_anchor, const int32_t* anch
 alr_status alr_ira_assemble(alr_ctx* ctx, int32_t n_primary, int32_t block,
                             const int32_t* tokens, const int32_t* top_ids, const float* top_logp,
                             const float* tail, int32_t n_secondary, const int32_t* sec_primary,
-                            const int32_t* sec_offset, float gamma, int32_t* token0_out,
-                            int32_t* top_ids_out, float* top_logp_out, float* tail_out,
-                            float* weight_out, alr_stream stream) {
+                            const int32_t* sec_offset, float gamma, int32_t eos_id,
+                            int32_t* token0_out, int32_t* top_ids_out, float* top_logp_out,
+                            float* tail_out, float* weight_out, alr_stream stream) {
   if (!ctx) return ALR_E_INVALID_ARG;
   if (n_primary <= 0 || n_primary > ctx->lim.max_anchors || block < 2 ||
       block > ctx->lim.max_block)
@@ -1256,8 +1297,22 @@ alr_status alr_ira_assemble(alr_ctx* ctx, int32_t n_primary, int32_t block,
   const long items = (long)n_secondary * block;
   ira_assemble_kernel<<<(unsigned)((items + 255) / 256), 256, 0, s>>>(
       dtab, dtab + n_secondary, n_secondary, block, tokens, top_ids, top_logp, tail, gamma,
-      token0_out, top_ids_out, top_logp_out, tail_out, weight_out);
+      eos_id, token0_out, top_ids_out, top_logp_out, tail_out, weight_out);
   ALR_LAUNCHED(ctx, "in-rollout anchor assembly");
+  return ALR_OK;
+}
+
+alr_status alr_slot_weights(alr_ctx* ctx, int32_t n, int32_t block, const int32_t* tokens,
+                            int32_t eos_id, float gamma, float* weight_out, alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (n < 0 || block < 1) return fail(ctx, ALR_E_INVALID_ARG, "n %d / block %d invalid", n, block);
+  if (!(gamma > 0.f)) return fail(ctx, ALR_E_INVALID_ARG, "gamma must be > 0");
+  if (n == 0) return ALR_OK;
+  if (!tokens || !weight_out) return fail(ctx, ALR_E_INVALID_ARG, "NULL pointer argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  slot_weights_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(tokens, n, block, eos_id, gamma,
+                                                                 weight_out);
+  ALR_LAUNCHED(ctx, "slot weights");
   return ALR_OK;
 }
 

@@ -61,6 +61,13 @@ def test_config_checks(lib):
     bad = binding.make_config(w.shape, w.max_pos)
     bad.dtype = 7
     assert lib.alr_check_config(ctypes.byref(bad), buf, 256) == 1
+    # multimodal RoPE sections: all zero, or non-negative with sum head_dim/2 (= 32 here)
+    ok = binding.make_config(W.scaled(w, "x", mrope_sections=(8, 12, 12)).shape, w.max_pos)
+    assert lib.alr_check_config(ctypes.byref(ok), buf, 256) == 0
+    for secs in ((8, 12, 11), (-2, 17, 17), (0, 0, 33)):
+        bad = binding.make_config(W.scaled(w, "x", mrope_sections=secs).shape, w.max_pos)
+        assert lib.alr_check_config(ctypes.byref(bad), buf, 256) == 1
+        assert b"mrope_sections" in buf.value
 
 
 def test_workspace_bytes_monotone_and_zero_on_invalid(lib):
