@@ -68,36 +68,100 @@ struct EpiQKV {
       Elt<OutT>::st(dst + cl + 32, hi);
     }
   }
-  // Rows row0 .. row0+nrow-1 (nrow <= 4) of columns c and c+32.  Four rows
-  // that are four consecutive, 4-aligned columns of the transposed V cache go
-  // out as one 8-byte store per column (bf16); everything else per element.
-  __device__ __forceinline__ void quad(int row0, int nrow, int c, const float* lo,
-                                       const float* hi) const {
-    if constexpr (std::is_same<OutT, bf16>::value) {
-      if (vt_col && c >= (H + G) * hd && nrow == 4) {
-        const int col0 = vt_col[row0];
-        if (vt_col[row0 + 3] == col0 + 3 && (col0 & 3) == 0) {
-          const long cl = c - (H + G) * hd;
-          u32x2 wl, wh;
-          wl[0] = pack2bf(lo[0], lo[1]);
-          wl[1] = pack2bf(lo[2], lo[3]);
-          wh[0] = pack2bf(hi[0], hi[1]);
-          wh[1] = pack2bf(hi[2], hi[3]);
-          *(u32x2*)(v + cl * vt_stride + col0) = wl;
-          *(u32x2*)(v + (cl + 32) * vt_stride + col0) = wh;
-          return;
-        }
+  // The 16 rows of a lane's 32-row block (row of index t: rb + 8 (t >> 2) +
+  // (t & 3); rows >= M are skipped) of columns c and c+32.  Every load the
+  // rows need (positions, then cos/sin, or the V^T columns) is issued before
+  // any store, so the block costs two memory round trips rather than one per
+  // row.  Four consecutive, 4-aligned columns of the transposed V cache go out
+  // as one 8-byte store per column (bf16).
+  __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
+                                         const float* hi) const {
+    const int half = hd >> 1;
+    const int qd = H * hd, kd = G * hd;
+    int r[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) r[t] = rb + 8 * (t >> 2) + (t & 3);
+    if (c < qd + kd) {
+      OutT* base;
+      long rs;
+      int cl;
+      if (c < qd) {
+        base = q;
+        rs = qd;
+        cl = c;
+      } else {
+        base = k;
+        rs = kv_rs;
+        cl = c - qd;
       }
+      const int f = 32 * (cl >> 6) + (cl & 63);
+      const int head = f / half, i = f - head * half;
+      const int axis = (i < sec0) ? 0 : ((i < sec01) ? 1 : 2);
+      int pp[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) pp[t] = pos[3 * min(r[t], M - 1) + axis];
+      float cs[16], sn[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const long o = (long)(pp[t] + pos_add) * half + i;
+        cs[t] = cosT[o];
+        sn[t] = sinT[o];
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t)
+        if (r[t] < M) {
+          OutT* dst = base + (long)r[t] * rs + head * hd + i;
+          Elt<OutT>::st(dst, lo[t] * cs[t] - hi[t] * sn[t]);
+          Elt<OutT>::st(dst + half, hi[t] * cs[t] + lo[t] * sn[t]);
+        }
+    } else if (vt_col) {
+      const long cl = c - qd - kd;
+      int col[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) col[t] = vt_col[min(r[t], M - 1)];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int t0 = 4 * g;
+        if constexpr (std::is_same<OutT, bf16>::value) {
+          if (r[t0 + 3] < M && col[t0 + 3] == col[t0] + 3 && (col[t0] & 3) == 0) {
+            u32x2 wl, wh;
+            wl[0] = pack2bf(lo[t0], lo[t0 + 1]);
+            wl[1] = pack2bf(lo[t0 + 2], lo[t0 + 3]);
+            wh[0] = pack2bf(hi[t0], hi[t0 + 1]);
+            wh[1] = pack2bf(hi[t0 + 2], hi[t0 + 3]);
+            *(u32x2*)(v + cl * vt_stride + col[t0]) = wl;
+            *(u32x2*)(v + (cl + 32) * vt_stride + col[t0]) = wh;
+            continue;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (r[t0 + e] < M) {
+            Elt<OutT>::st(v + cl * vt_stride + col[t0 + e], lo[t0 + e]);
+            Elt<OutT>::st(v + (cl + 32) * vt_stride + col[t0 + e], hi[t0 + e]);
+          }
+      }
+    } else {
+      const int cl = c - qd - kd;
+#pragma unroll
+      for (int t = 0; t < 16; ++t)
+        if (r[t] < M) {
+          OutT* dst = v + (long)r[t] * kv_rs;
+          Elt<OutT>::st(dst + cl, lo[t]);
+          Elt<OutT>::st(dst + cl + 32, hi[t]);
+        }
     }
-    for (int i = 0; i < nrow; ++i) (*this)(row0 + i, c, lo[i], hi[i]);
   }
 };
 
-// Epilogues that handle four rows of a column pair at once define quad().
+// Epilogues that read memory define rows16(): a lane's 16 rows of a 32-row
+// block at once, all loads before all stores (the compiler cannot prove that a
+// later row's load does not alias an earlier row's store, so element-wise
+// calls would wait for one load round trip per row).
 template <class Epi, class = void>
-struct has_quad : std::false_type {};
+struct has_rows16 : std::false_type {};
 template <class Epi>
-struct has_quad<Epi, decltype((void)&Epi::quad)> : std::true_type {};
+struct has_rows16<Epi, decltype((void)&Epi::rows16)> : std::true_type {};
 
 // Residual add into the fp32 stream, optionally capturing the new value as a
 // feature row: feat + (perm ? perm[row] : row) * feat_rs.
@@ -119,6 +183,35 @@ struct EpiResid {
       f[32] = b;
     }
   }
+  __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
+                                         const float* hi) const {
+    int r[16];
+    long fr[16];
+    float a[16], b[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      r[t] = rb + 8 * (t >> 2) + (t & 3);
+      const int rc = min(r[t], M - 1);
+      const float* p = h + (long)rc * ld + c;
+      a[t] = p[0];
+      b[t] = p[32];
+      fr[t] = (feat && perm) ? perm[rc] : r[t];
+    }
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      if (r[t] < M) {
+        a[t] += lo[t];
+        b[t] += hi[t];
+        float* p = h + (long)r[t] * ld + c;
+        p[0] = a[t];
+        p[32] = b[t];
+        if (feat) {
+          float* f = feat + fr[t] * feat_rs + c;
+          f[0] = a[t];
+          f[32] = b[t];
+        }
+      }
+  }
 };
 
 // SwiGLU: 64-column group t holds gate rows 32t..32t+31 then up rows
@@ -129,7 +222,9 @@ struct EpiSwiGLU {
   int ld;
   __device__ __forceinline__ void operator()(int row, int c, float g, float u) const {
     const int col = (c >> 6) * 32 + (c & 63);
-    const float s = g / (1.0f + expf(-g));
+    // SiLU(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
+    // 2 ulp of fp32; e^-g overflowing to inf gives the limit 0)
+    const float s = g * __builtin_amdgcn_rcpf(1.0f + fast_exp2(-1.44269504088896341f * g));
     Elt<OutT>::st(out + (long)row * ld + col, s * u);
   }
 };
@@ -145,12 +240,30 @@ struct EpiLogits {
     p[0] = lo;
     p[32] = hi;
   }
+  __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
+                                         const float* hi) const {
+    int r[16];
+    long rr[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      r[t] = rb + 8 * (t >> 2) + (t & 3);
+      rr[t] = perm ? perm[min(r[t], M - 1)] : r[t];
+    }
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      if (r[t] < M) {
+        float* p = out + rr[t] * rs + c;
+        p[0] = lo[t];
+        p[32] = hi[t];
+      }
+  }
 };
 
 // Epilogue of a wave's MI x NI block of 32x32 accumulators whose top-left
 // output is (row0, col0): lane (lr, lh) of block (mi, nj) holds rows row0 +
 // 32 mi + 8 q + 4 lh + e (q, e = 0..3; register 4 q + e) of columns col0 +
-// 64 nj + lr and that + 32 (accumulators 2 nj and 2 nj + 1).
+// 64 nj + lr and that + 32 (accumulators 2 nj and 2 nj + 1).  Epilogues with
+// a rows16() form get those 16 rows in one call.
 template <int MI, int NI, class Epi>
 __device__ __forceinline__ void gemm_store_tile(const Epi& epi, const f32x16 (&acc)[MI][NI],
                                                 int row0, int col0, int M, int N) {
@@ -160,26 +273,28 @@ __device__ __forceinline__ void gemm_store_tile(const Epi& epi, const f32x16 (&a
     const int col = col0 + nj * 64 + lr;
     if (col < N) {
 #pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
+      for (int mi = 0; mi < MI; ++mi) {
+        if constexpr (has_rows16<Epi>::value) {
+          const int rb = row0 + mi * 32 + 4 * lh;
+          if (rb < M) {
+            float lo[16], hi[16];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = row0 + mi * 32 + 8 * q + 4 * lh;
-          if constexpr (has_quad<Epi>::value) {
-            if (row < M) {
-              float lo[4], hi[4];
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                lo[e] = acc[mi][2 * nj][4 * q + e];
-                hi[e] = acc[mi][2 * nj + 1][4 * q + e];
-              }
-              epi.quad(row, min(4, M - row), col, lo, hi);
+            for (int t = 0; t < 16; ++t) {
+              lo[t] = acc[mi][2 * nj][t];
+              hi[t] = acc[mi][2 * nj + 1][t];
             }
-          } else {
+            epi.rows16(rb, M, col, lo, hi);
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = row0 + mi * 32 + 8 * q + 4 * lh;
 #pragma unroll
             for (int e = 0; e < 4; ++e)
               if (row + e < M) epi(row + e, col, acc[mi][2 * nj][4 * q + e], acc[mi][2 * nj + 1][4 * q + e]);
           }
         }
+      }
     }
   }
 }
