@@ -354,7 +354,13 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     // Split-K over the 256x256 ping-pong kernel when its tiles leave CUs idle:
     // the largest slice count in {2, 4} that keeps one workgroup per CU, K
     // slices of >= 512 and a multiple of 64, and the partial sums in the buffer.
-    if ((cfg == 0 || cfg == 18) && ctx->splitk_buf != nullptr) {
+    // Where 128x128 tiles alone give every CU the same number of tiles and
+    // K <= 4096, writing and re-reading the fp32 partial sums costs more than
+    // the ping-pong kernel gains (M = 1024, N = 4096: 46 vs 55 us), so those
+    // GEMMs take the 128x128 kernel with the epilogue fused.  With uneven
+    // rounds (N = 6144: 384 tiles on 256 CUs) split-K stays ahead.
+    const bool fill128 = K <= 4096 && tiles(128, 128) % ctx->n_cu == 0;
+    if ((cfg == 18 || (cfg == 0 && !fill128)) && ctx->splitk_buf != nullptr) {
       const int t256 = tiles(256, 256);
       int S = 1;
       for (int cand : {2, 4})
