@@ -31,7 +31,10 @@ extern "C" {
  * phases): 15 = 256x256 (4 stages), 16 = 256x256 (5 stages); 17 = ping-pong
  * over register-staged BK = 64 tiles (K a multiple of 64); 18 = split-K over
  * the ping-pong kernel (K slices summed in slice order by a second kernel;
- * 2 or 4 slices by the library's rule, at least 2; K a multiple of 128).
+ * 2 or 4 slices by the library's rule, at least 2; K a multiple of 128);
+ * 19 = the ping-pong kernel of 17 run persistently (one workgroup per CU
+ * looping over the tiles, the next tile's first k-steps loaded during the
+ * current tile's last ones).
  * Tiles 6..8 need a device scratch buffer of N*K*2 + N*8 bytes to hold the
  * pre-shuffled W (the call then synchronises `stream` once after
  * shuffling); tile 18 needs one of at least 2*M*N*4 bytes for the partial

@@ -183,34 +183,41 @@ struct EpiResid {
       f[32] = b;
     }
   }
+  // In two halves of 8 rows (loads, then stores), which bounds the registers
+  // the epilogue needs inside a persistent kernel.
   __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
                                          const float* hi) const {
-    int r[16];
-    long fr[16];
-    float a[16], b[16];
 #pragma unroll
-    for (int t = 0; t < 16; ++t) {
-      r[t] = rb + 8 * (t >> 2) + (t & 3);
-      const int rc = min(r[t], M - 1);
-      const float* p = h + (long)rc * ld + c;
-      a[t] = p[0];
-      b[t] = p[32];
-      fr[t] = (feat && perm) ? perm[rc] : r[t];
-    }
+    for (int half = 0; half < 2; ++half) {
+      int fr[8];
+      float a[8], b[8];
 #pragma unroll
-    for (int t = 0; t < 16; ++t)
-      if (r[t] < M) {
-        a[t] += lo[t];
-        b[t] += hi[t];
-        float* p = h + (long)r[t] * ld + c;
-        p[0] = a[t];
-        p[32] = b[t];
-        if (feat) {
-          float* f = feat + fr[t] * feat_rs + c;
-          f[0] = a[t];
-          f[32] = b[t];
+      for (int u = 0; u < 8; ++u) {
+        const int t = 8 * half + u;
+        const int r = rb + 8 * (t >> 2) + (t & 3), rc = min(r, M - 1);
+        const float* p = h + (long)rc * ld + c;
+        a[u] = p[0];
+        b[u] = p[32];
+        fr[u] = (feat && perm) ? perm[rc] : r;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int t = 8 * half + u;
+        const int r = rb + 8 * (t >> 2) + (t & 3);
+        if (r < M) {
+          a[u] += lo[t];
+          b[u] += hi[t];
+          float* p = h + (long)r * ld + c;
+          p[0] = a[u];
+          p[32] = b[u];
+          if (feat) {
+            float* f = feat + (long)fr[u] * feat_rs + c;
+            f[0] = a[u];
+            f[32] = b[u];
+          }
         }
       }
+    }
   }
 };
 
@@ -242,17 +249,16 @@ struct EpiLogits {
   }
   __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
                                          const float* hi) const {
-    int r[16];
-    long rr[16];
+    int rr[16];
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
-      r[t] = rb + 8 * (t >> 2) + (t & 3);
-      rr[t] = perm ? perm[min(r[t], M - 1)] : r[t];
+      const int r = rb + 8 * (t >> 2) + (t & 3);
+      rr[t] = perm ? perm[min(r, M - 1)] : r;
     }
 #pragma unroll
     for (int t = 0; t < 16; ++t)
-      if (r[t] < M) {
-        float* p = out + rr[t] * rs + c;
+      if (rb + 8 * (t >> 2) + (t & 3) < M) {
+        float* p = out + (long)rr[t] * rs + c;
         p[0] = lo[t];
         p[32] = hi[t];
       }
@@ -925,6 +931,131 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp64_kernel(
   if (grp == 0) __builtin_amdgcn_s_barrier();
 
   gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
+}
+
+// ------------------------------------------------------------------ bf16 MFMA GEMM, ping-pong, persistent
+//
+// gemm_bf16_pp64_kernel's schedule run by one workgroup per CU over tiles
+// blockIdx.x, blockIdx.x + gridDim.x, ...  The k-steps of consecutive tiles
+// form one stream: in the last two k-steps of a tile the global loads already
+// fetch the next tile's first two steps, and the LDS stage parity runs on
+// across tiles.  A group's epilogue sits between its last compute phase of a
+// tile and its first memory phase of the next, i.e. while the other group
+// computes, so the pipeline is neither drained nor refilled between tiles.
+template <int TAG, class Epi>
+__global__ __launch_bounds__(512, 1) void gemm_bf16_pp64p_kernel(
+    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
+    int tiles_m, int tiles_n, Epi epi) {
+  constexpr int BM = 256, BN = 256, BK = 64;
+  constexpr int WTM = 128, WTN = 64, MI = 4, NI = 2;
+  constexpr int STAGE = (BM + BN) * BK;  // bf16 elements
+  __shared__ __attribute__((aligned(1024))) bf16 smem[2 * STAGE];
+
+  const int ntiles = tiles_m * tiles_n;
+  int tile = blockIdx.x;
+  if (tile >= ntiles) return;  // uniform over the workgroup
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
+  const int wm = grp, wn = wave & 3;
+  const int nk = K / BK;
+
+  // thread t moves chunks t + 512 i (row ch >> 3, 16-byte chunk ch & 7) of
+  // the A tile (half 0) and of the W tile (half 1)
+  int loff[2][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ch = tid + 512 * i, r = ch >> 3, c = ch & 7;
+    loff[0][i] = swz<BK>(r, c);
+    loff[1][i] = BM * BK + swz<BK>(r, c);
+  }
+  auto offsets = [&](int t, uint32_t (&go)[2][4]) {
+    int tm, tn;
+    gemm_tile_coords(t, tiles_m, tiles_n, tm, tn);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ch = tid + 512 * i, r = ch >> 3, c = ch & 7;
+      go[0][i] = (uint32_t)(((long)min(tm * BM + r, M - 1) * lda + c * 8) * 2);
+      go[1][i] = (uint32_t)(((long)min(tn * BN + r, N - 1) * ldw + c * 8) * 2);
+    }
+  };
+  uint32_t gcur[2][4], gnxt[2][4];
+  int next = tile + gridDim.x;
+  offsets(tile, gcur);
+  offsets(next < ntiles ? next : tile, gnxt);
+  const char* gbase[2] = {(const char*)A, (const char*)W};
+  // step s of the stream relative to the current tile: s < nk is the current
+  // tile, s >= nk the next one (or the current tile's last step when there is
+  // none; those loads are never used)
+  auto gload = [&](GemmRegs<4>& rg, int h, int s) {
+    const bool nx = s >= nk;
+    const int st = nx ? (next < ntiles ? s - nk : nk - 1) : s;
+    const char* b = gbase[h] + (long)st * BK * 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rg.v[i] = *(const u32x4*)(b + (nx ? gnxt[h][i] : gcur[h][i]));
+  };
+  auto lstore = [&](const GemmRegs<4>& rg, int h, bf16* stage) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *(u32x4*)(stage + loff[h][i]) = rg.v[i];
+  };
+
+  GemmRegs<4> rg[2];
+  gload(rg[0], 0, 0);
+  gload(rg[1], 1, 0);
+  lstore(rg[0], 0, smem);
+  lstore(rg[1], 1, smem);
+  gload(rg[0], 0, 1);
+  gload(rg[1], 1, 1);
+  __syncthreads();
+  if (grp == 1) __builtin_amdgcn_s_barrier();  // group 1 runs one phase behind
+
+  f32x16 acc[MI][NI];
+  GemmFrag<MI, NI> f0, f1;
+  int gs = 0;  // k-steps done by this workgroup over all its tiles
+  while (true) {
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
+    for (int kt = 0; kt < nk; ++kt, ++gs) {
+      const bf16* cur = smem + (gs & 1) * STAGE;
+      bf16* nxt = smem + ((gs + 1) & 1) * STAGE;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // memory phase
+        __builtin_amdgcn_sched_barrier(0);
+        gemm_frag_load<BK, MI, NI, WTM, WTN>(f0, cur, cur + BM * BK, wm, wn, 2 * h);
+        gemm_frag_load<BK, MI, NI, WTM, WTN>(f1, cur, cur + BM * BK, wm, wn, 2 * h + 1);
+        lstore(rg[h], h, nxt);
+        gload(rg[h], h, kt + 2);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): fragments read, stage writes done
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // compute phase
+        __builtin_amdgcn_s_setprio(1);
+        gemm_frag_mma<MI, NI>(f0, acc);
+        gemm_frag_mma<MI, NI>(f1, acc);
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();
+      }
+    }
+    int tm, tn;
+    gemm_tile_coords(tile, tiles_m, tiles_n, tm, tn);
+    gemm_store_tile<MI, NI>(epi, acc, tm * BM + wm * WTM, tn * BN + wn * WTN, M, N);
+    if (next >= ntiles) break;
+    tile = next;
+    next = tile + gridDim.x;
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gcur[hh][i] = gnxt[hh][i];
+    if (next < ntiles) offsets(next, gnxt);
+  }
+  if (grp == 0) __builtin_amdgcn_s_barrier();
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM, 3-stage LDS ring

@@ -345,9 +345,9 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
   if (M <= 0) return;
   ProfScope ps(ctx, TAG, st);
   if constexpr (std::is_same<T, bf16>::value) {
-    // W row-major.  256x256 ping-pong (BK = 64) for the prefill and wide decode
-    // GEMMs, 128x128 (then 64x128) LDS-staged tiles where 256x256 would leave
-    // CUs idle.  force_tile (debug hook only) picks any variant; 6..8 need W
+    // W row-major.  256x256 ping-pong (BK = 64), persistent over the tiles, for
+    // the prefill and wide decode GEMMs, 128x128 (then 64x128) LDS-staged tiles
+    // where 256x256 would leave CUs idle.  force_tile (debug hook only) picks any variant; 6..8 need W
     // pre-shuffled.
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     int cfg = force_tile;
@@ -381,12 +381,12 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
       if (cfg == 18) cfg = 0;
     }
     if (cfg == 0)
-      cfg = tiles(256, 256) >= 256 ? ((K % 64) == 0 ? 17 : 4) : (tiles(128, 128) >= 256 ? 2 : 3);
+      cfg = tiles(256, 256) >= 256 ? ((K % 64) == 0 ? 19 : 4) : (tiles(128, 128) >= 256 ? 2 : 3);
     // the direct-to-LDS kernels address operands with 32-bit byte offsets
     const bool dma_ok = (K % 32) == 0 && ((size_t)(M - 1) * lda + K) * 2 <= 0xFFFFFFFFull &&
                         ((size_t)(N - 1) * ldw + K) * 2 <= 0xFFFFFFFFull;
     if (cfg >= 11 && cfg <= 16 && !dma_ok) cfg = 4;
-    if (cfg == 17 && (K % 64) != 0) cfg = 4;
+    if ((cfg == 17 || cfg == 19) && (K % 64) != 0) cfg = 4;
     const bool k64 = (K % 128) == 0;
     const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8 || cfg == 9 ||
                     (cfg >= 11 && cfg <= 13) || cfg >= 15)
@@ -420,6 +420,10 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         break;
       case 17:
         gemm_bf16_pp64_kernel<TAG, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
+        break;
+      case 19:
+        gemm_bf16_pp64p_kernel<TAG, Epi>
+            <<<std::min(nb, ctx->n_cu), 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
         break;
       case 9: ALR_GEMM_R3(256, 256, 2, 4, 1); break;
       case 10: ALR_GEMM_R3(128, 128, 2, 2, 2); break;
@@ -1339,7 +1343,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || tile > 18) return ALR_E_INVALID_ARG;
+  if (tile < 0 || tile > 19) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
