@@ -462,14 +462,14 @@ struct DecodeGroup {
 // 64/(HD/8) heads and a score is a reduction over those lanes.  The private
 // key and value rows of the kv head are read by every head of the pass.
 template <int HD>
-__global__ __launch_bounds__(256) void attn_decode_combine_kernel(
+__global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
     const int* __restrict__ grp_of_row, const DecodeGroup* __restrict__ groups,
     const float* __restrict__ part_o, const float* __restrict__ part_ml,
     const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     long priv_rs, int n_priv, bf16* __restrict__ O, int n_rows, AttnGeom g) {
   constexpr int LPH = HD / 8;    // lanes per head
   constexpr int HPP = 64 / LPH;  // heads per pass
-  constexpr int PB = 16;         // private keys per block
+  constexpr int PB = 8;          // private keys per block (bounds the registers: 4 waves per SIMD)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const long item = (long)blockIdx.x * 4 + wave;
   if (item >= (long)n_rows * g.G) return;  // no barrier in this kernel
