@@ -33,27 +33,62 @@ __global__ __launch_bounds__(256) void embed_kernel(float* __restrict__ resid,
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Elt<T>::ld(src + c);
 }
 
-// out[r, :] = x[r, :] * g / sqrt(mean(x[r, :]^2) + eps)
+// out[c .. c+3] = v * inv * g[c .. c+3], four elements at once
+__device__ __forceinline__ void norm4(float* o, f32x4 v, const float* g, float inv) {
+  const f32x4 gv = *(const f32x4*)g;
+  f32x4 w;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) w[e] = v[e] * inv * gv[e];
+  *(f32x4*)o = w;
+}
+__device__ __forceinline__ void norm4(bf16* o, f32x4 v, const bf16* g, float inv) {
+  const u32x2 gw = *(const u32x2*)g;
+  float gf[4];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    gf[2 * e] = bf2f((bf16)(gw[e] & 0xFFFFu));
+    gf[2 * e + 1] = bf2f((bf16)(gw[e] >> 16));
+  }
+  u32x2 w;
+  w[0] = pack2bf(v[0] * inv * gf[0], v[1] * inv * gf[1]);
+  w[1] = pack2bf(v[2] * inv * gf[2], v[3] * inv * gf[3]);
+  *(u32x2*)o = w;
+}
+
+// out[r, :] = x[r, :] * g / sqrt(mean(x[r, :]^2) + eps); d a multiple of 4.  The
+// row stays in registers between the two passes for d <= 8192.
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
                                                       const T* __restrict__ g,
                                                       T* __restrict__ out, int d, float eps) {
+  constexpr int CACHE = 8;  // 4-element chunks per thread held in registers
   __shared__ float red[4];
   const long r = blockIdx.x;
   const float* xr = x + r * d;
+  T* o = out + r * d;
+  f32x4 v[CACHE];
   float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    const f32x4 v = *(const f32x4*)(xr + c);
-    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+#pragma unroll
+  for (int k = 0; k < CACHE; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) {
+      v[k] = *(const f32x4*)(xr + c);
+      ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
+    }
+  }
+  for (int c = (threadIdx.x + 256 * CACHE) * 4; c < d; c += 1024) {
+    const f32x4 w = *(const f32x4*)(xr + c);
+    ss += w[0] * w[0] + w[1] * w[1] + w[2] * w[2] + w[3] * w[3];
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  T* o = out + r * d;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    const f32x4 v = *(const f32x4*)(xr + c);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) Elt<T>::st(o + c + e, v[e] * inv * Elt<T>::ld(g + c + e));
+  for (int k = 0; k < CACHE; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) norm4(o + c, v[k], g + c, inv);
   }
+  for (int c = (threadIdx.x + 256 * CACHE) * 4; c < d; c += 1024)
+    norm4(o + c, *(const f32x4*)(xr + c), g + c, inv);
 }
 
 // dst[r, :] = src[idx[r], :]  (row_elems elements of T)
