@@ -20,25 +20,18 @@ extern "C" {
  * for `dtype` (ALR_BF16: bf16 MFMA with fp32 accumulation; ALR_F32: fp32 FMA).
  * A, W, C are device pointers, row-major and contiguous; N and K must be
  * multiples of 64 (ALR_E_UNSUPPORTED otherwise).  `tile` picks the bf16
- * kernel: 0 = the library's choice for this shape; W read from registers
- * (pre-shuffled): 6 = 256x256 (8 waves), 7 = 128x128, 8 = 256x128; W staged
- * through LDS: 1 = 256x128, 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves),
- * 5 = 256x256 (4 waves); three-stage LDS ring: 9 = 256x256 (8 waves),
- * 10 = 128x128; operands loaded straight into an LDS ring (no register
- * staging): 11 = 256x256 (8 waves, 4 stages), 12 = 256x256 (8 waves,
- * 5 stages), 13 = 256x256 (4 waves, 4 stages), 14 = 128x128 (4 stages);
- * ping-pong (the two waves of each SIMD alternate LDS/transfer and MFMA
- * phases): 15 = 256x256 (4 stages), 16 = 256x256 (5 stages); 17 = ping-pong
- * over register-staged BK = 64 tiles (K a multiple of 64); 18 = split-K over
- * the ping-pong kernel (K slices summed in slice order by a second kernel;
- * 2 or 4 slices by the library's rule, at least 2; K a multiple of 128);
- * 19 = the ping-pong kernel of 17 run persistently (one workgroup per CU
- * looping over the tiles, the next tile's first k-steps loaded during the
- * current tile's last ones).
- * Tiles 6..8 need a device scratch buffer of N*K*2 + N*8 bytes to hold the
- * pre-shuffled W (the call then synchronises `stream` once after
- * shuffling); tile 18 needs one of at least 2*M*N*4 bytes for the partial
- * sums (up to 4*M*N*4 are used when given); ALR_E_WORKSPACE otherwise.
+ * kernel: 0 = the library's choice for this shape; W staged through LDS:
+ * 1 = 256x128, 2 = 128x128, 3 = 64x128, 4 = 256x256 (8 waves), 5 = 256x256
+ * (4 waves); 17 = ping-pong (the two waves of each SIMD alternate LDS and
+ * MFMA phases) over register-staged BK = 64 tiles, one tile per workgroup
+ * (K a multiple of 64); 18 = split-K over the ping-pong kernel (K slices
+ * summed in slice order by a second kernel; 2 or 4 slices by the library's
+ * rule, at least 2; K a multiple of 128); 19 = the ping-pong kernel of 17 run
+ * persistently (one workgroup per CU looping over the tiles, the next tile's
+ * first k-steps loaded during the current tile's last ones).  Other values:
+ * ALR_E_INVALID_ARG.  Tile 18 needs a device scratch buffer of at least
+ * 2*M*N*4 bytes for the partial sums (up to 4*M*N*4 are used when given);
+ * ALR_E_WORKSPACE otherwise.
  * Enqueued on `stream`. */
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
                           int32_t N, int32_t K, int32_t tile, void* scratch,

@@ -400,9 +400,6 @@ def debug_gemm(dtype: int, A, W, C, stream=None, tile: int = 0):
     N = W.shape[0]
     scratch = None
     nbytes = 0
-    if dtype == ALR_BF16 and 6 <= tile <= 8:
-        nbytes = N * K * 2 + N * 8
-        scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
     if dtype == ALR_BF16 and tile == 18:
         nbytes = 4 * M * N * 4
         scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)

@@ -1,12 +1,13 @@
 // GEMM kernels C[M,N] = A[M,K] * W[N,K]^T with fused epilogues (gfx950).
 //
 // bf16 path: 32x32x16 bf16 MFMA with fp32 accumulation.  Large GEMMs use the
-// 256x256 ping-pong kernel over register-staged BK = 64 tiles
-// (gemm_bf16_pp64_kernel); GEMMs with fewer than 256 such tiles use the
-// LDS-staged gemm_bf16_kernel at 128x128 or 64x128.  The other variants
-// (direct-to-LDS rings, W from registers, 3-stage ring) are reachable through
-// the debug entry point for comparison.  fp32 path: FMA, 64x64x16 tile.  Both hand the epilogue *pairs* of outputs: the value at column c and
-// the one at column c+32, where c lies in the low half of a 64-column group.
+// 256x256 ping-pong kernel over register-staged BK = 64 tiles, run
+// persistently (gemm_bf16_pp64p_kernel; gemm_bf16_pp64_kernel is the same
+// schedule one tile per workgroup, used for split-K); GEMMs with fewer than
+// 256 such tiles use the LDS-staged gemm_bf16_kernel at 128x128 or 64x128.
+// fp32 path: FMA, 64x64x16 tile.  Both hand the epilogue *pairs* of outputs:
+// the value at column c and the one at column c+32, where c lies in the low
+// half of a 64-column group.
 // Weight rows are arranged at context creation so that every fused operation
 // needs exactly such a pair: SwiGLU's gate/up values and RoPE's rotate-half
 // partners (i, i + head_dim/2) land 32 columns apart in the same lane.
@@ -442,15 +443,6 @@ __device__ __forceinline__ void gemm_frag_mma(const GemmFrag<MI, NI>& f,
     for (int ni = 0; ni < NI; ++ni) acc[mi][ni] = mfma32x32x16(f.a[mi], f.b[ni], acc[mi][ni]);
 }
 
-// Part P of NP of the MFMAs of one k-slice (NP divides MI*NI).
-template <int MI, int NI, int P, int NP>
-__device__ __forceinline__ void gemm_frag_mma_part(const GemmFrag<MI, NI>& f,
-                                                   f32x16 (&acc)[MI][NI]) {
-  constexpr int T = MI * NI, B = P * T / NP, E = (P + 1) * T / NP;
-#pragma unroll
-  for (int t = B; t < E; ++t) acc[t / NI][t % NI] = mfma32x32x16(f.a[t / NI], f.b[t % NI], acc[t / NI][t % NI]);
-}
-
 // MFMAs of one LDS stage, k-slice by k-slice, reading the fragments of slice
 // ks+1 while slice ks runs, and writing the next step's operand registers
 // (ra, rw) into the other LDS stage a few chunks per slice so the LDS writes
@@ -556,262 +548,6 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
                                                      Ws[0], a_off, w_off);
     __syncthreads();
   }
-
-  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
-}
-
-// ------------------------------------------------------------------ bf16 MFMA GEMM, direct-to-LDS ring
-//
-// Operand tiles go from global memory straight into LDS (global_load_lds_dwordx4:
-// lane i of a wave writes the 16 bytes it fetched to LDS address M0 + 16 i), so
-// no VGPRs hold staged operands and no ds_write is issued.  Which global chunk a
-// lane fetches is chosen so that the 1 KB each instruction writes is a block of
-// the XOR-swizzled layout the fragment reads expect (rows of BK = 32 bf16, 4
-// chunks of 16 B, swizzle as swz<32>).
-//
-// NS LDS stages form a ring.  Iteration kt computes step kt from stage kt % NS
-// and issues the loads of step kt+NS-1 into the stage step kt-1 used.  At the
-// end of the iteration each wave waits for its own loads of step kt+2 and the
-// workgroup barrier publishes them, so during iteration kt both step kt and step
-// kt+1 are readable: the first k-slice of step kt+1 is read into registers
-// while the second k-slice of step kt runs, and no wave starts an iteration
-// waiting for LDS.  Loads are in flight for about NS-3 iterations.  Steps past
-// the end are clamped to the last one and land in stages nobody reads again, so
-// every iteration issues the same number of loads and the fixed vmcnt waits
-// stay exact.  The compiler does not see these loads (inline asm), so every wait
-// on them is explicit, including the final one before the workgroup may exit.
-
-__device__ __forceinline__ uint32_t lds_byte_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// One wave-wide 1 KB transfer: lane i copies 16 B from gbase + voff to LDS m0 + 16 i.
-__device__ __forceinline__ void dma_1k(uint32_t m0, uint32_t voff, const void* gbase) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :
-               : "s"(m0), "v"(voff), "s"(gbase)
-               : "memory", "m0");
-}
-
-// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-template <int TAG, int BM, int BN, int WGM, int WGN, int NS, int OCC, class Epi>
-__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_dma_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
-  constexpr int BK = 32;
-  constexpr int NT = 64 * WGM * WGN, NW = NT / 64;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
-  constexpr int MI = WTM / 32, NI = WTN / 32;
-  constexpr int A_DMA = BM * 4 / NT, W_DMA = BN * 4 / NT;  // 1 KB transfers per wave per step
-  static_assert(A_DMA * NT == BM * 4 && W_DMA * NT == BN * 4, "tile does not split into 1 KB blocks");
-  constexpr int A_BYTES = BM * BK * 2, STAGE_BYTES = (BM + BN) * BK * 2;
-  static_assert(NS >= 4, "the ring needs four stages");
-  __shared__ __attribute__((aligned(1024))) bf16 smem[NS * (BM + BN) * BK];
-
-  int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave / WGN, wn = wave % WGN;
-
-  // Transfer j of this wave covers LDS slots (j*NW + wave)*64 + lane of its
-  // operand region; slot p holds row p/4, chunk (p%4) ^ h(row).
-  uint32_t a_voff[A_DMA], w_voff[W_DMA];
-#pragma unroll
-  for (int j = 0; j < A_DMA; ++j) {
-    const int p = (j * NW + wave) * 64 + lane, r = p >> 2;
-    const int c = (swz<BK>(r, p & 3) & 31) >> 3;  // the XOR is an involution
-    a_voff[j] = (uint32_t)(((long)min(m0 + r, M - 1) * lda + c * 8) * 2);
-  }
-#pragma unroll
-  for (int j = 0; j < W_DMA; ++j) {
-    const int p = (j * NW + wave) * 64 + lane, r = p >> 2;
-    const int c = (swz<BK>(r, p & 3) & 31) >> 3;
-    w_voff[j] = (uint32_t)(((long)min(n0 + r, N - 1) * ldw + c * 8) * 2);
-  }
-  const uint32_t lds0 = lds_byte_addr(smem);
-  const int nk = K / BK;
-
-  // transfer q (A blocks first, then W) of step `step` into ring stage `stage`
-  auto issue_one = [&](int q, int step, int stage) {
-    const int s = min(step, nk - 1);
-    const uint32_t base = lds0 + stage * STAGE_BYTES;
-    if (q < A_DMA)
-      dma_1k(base + (q * NW + wave) * 1024, a_voff[q], (const char*)A + (long)s * BK * 2);
-    else
-      dma_1k(base + A_BYTES + ((q - A_DMA) * NW + wave) * 1024, w_voff[q - A_DMA],
-             (const char*)W + (long)s * BK * 2);
-  };
-  auto issue = [&](int step, int stage) {
-#pragma unroll
-    for (int q = 0; q < A_DMA + W_DMA; ++q) issue_one(q, step, stage);
-  };
-  // Each k-slice's MFMAs run in groups with one transfer issued before each
-  // group: the workgroup's waves leave the barrier together, and issuing all
-  // transfers at once would fill the address unit's queue and stall the
-  // MFMAs queued behind them in every wave.
-  constexpr int DPS = (A_DMA + W_DMA) / 2;  // transfers per k-slice
-  static_assert(DPS * 2 == A_DMA + W_DMA && (MI * NI) % DPS == 0, "transfer split");
-  auto stage_ptr = [&](int stage) { return smem + stage * (STAGE_BYTES / 2); };
-
-#pragma unroll
-  for (int s = 0; s < NS - 1; ++s) issue(s, s);
-  wait_vmcnt<(NS - 3) * (A_DMA + W_DMA)>();  // steps 0 and 1 landed (this wave)
-  __syncthreads();
-
-  f32x16 acc[MI][NI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-
-  GemmFrag<MI, NI> f0, f1;
-  gemm_frag_load<BK, MI, NI, WTM, WTN>(f0, stage_ptr(0), stage_ptr(0) + BM * BK, wm, wn, 0);
-  int cur = 0;  // stage of step kt
-  for (int kt = 0; kt < nk; ++kt) {
-    const int nxt = cur + 1 == NS ? 0 : cur + 1;
-    const int fill = cur == 0 ? NS - 1 : cur - 1;  // stage step kt-1 used
-    const bf16* As = stage_ptr(cur);
-    const bf16* An = stage_ptr(nxt);
-    // each slice: issue its LDS reads first, then the MFMAs that hide them,
-    // with the step's transfers spread over the MFMA groups
-    gemm_frag_load<BK, MI, NI, WTM, WTN>(f1, As, As + BM * BK, wm, wn, 1);
-    __builtin_amdgcn_sched_barrier(0);
-    static_for<DPS>([&](auto p) {
-      issue_one(p.value, kt + NS - 1, fill);
-      __builtin_amdgcn_sched_barrier(0);
-      gemm_frag_mma_part<MI, NI, p.value, DPS>(f0, acc);
-      __builtin_amdgcn_sched_barrier(0);
-    });
-    gemm_frag_load<BK, MI, NI, WTM, WTN>(f0, An, An + BM * BK, wm, wn, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    static_for<DPS>([&](auto p) {
-      issue_one(DPS + p.value, kt + NS - 1, fill);
-      __builtin_amdgcn_sched_barrier(0);
-      gemm_frag_mma_part<MI, NI, p.value, DPS>(f1, acc);
-      __builtin_amdgcn_sched_barrier(0);
-    });
-    wait_vmcnt<(NS - 3) * (A_DMA + W_DMA)>();  // this wave's loads of step kt+2 landed
-    __syncthreads();
-    cur = nxt;
-  }
-  wait_vmcnt<0>();  // no transfer may still target this workgroup's LDS
-
-  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
-}
-
-// ------------------------------------------------------------------ bf16 MFMA GEMM, ping-pong
-//
-// 256x256 tile, 8 waves, BK = 32, operands loaded straight into an NS-stage
-// LDS ring as in gemm_bf16_dma_kernel.  Waves are dealt to the four SIMDs
-// round-robin, so waves 0-3 (group 0) and 4-7 (group 1) put one wave of each
-// group on every SIMD.  Group g owns output rows [128 g, 128 g + 128) (wave
-// tile 128x64) and alternates two kinds of phase, separated by workgroup
-// barriers: a memory phase (read the whole step's fragments from LDS into
-// registers, issue its share of a later step's global->LDS transfers) and a
-// compute phase (the step's 16 MFMAs from registers only).  Group 1 starts one
-// barrier later, so in every phase one wave per SIMD computes while the other
-// loads, and the MFMA stream of a SIMD continues across each barrier.
-//
-// Phase 2s: group 0 reads step s, group 1 computes step s-1; phase 2s+1:
-// group 0 computes step s, group 1 reads step s.  Step s+NS-1 is loaded (half
-// by each group, in its memory phase of step s) into the stage step s-1 used,
-// which both groups finished reading before.  Before the barrier that opens
-// phase 2s+2 every wave has waited for its own transfers of step s+1.
-
-template <int TAG, int NS, class Epi>
-__global__ __launch_bounds__(512, 1) void gemm_bf16_pp_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
-  constexpr int BM = 256, BN = 256, BK = 32;
-  constexpr int WTM = 128, WTN = 64, MI = 4, NI = 2;
-  constexpr int D = NS - 1;  // steps whose transfers are in flight
-  constexpr int A_BYTES = BM * BK * 2, STAGE_BYTES = (BM + BN) * BK * 2;
-  constexpr int TPS = 4;  // 1 KB transfers per wave per step
-  static_assert(NS >= 3, "ring too short");
-  __shared__ __attribute__((aligned(1024))) bf16 smem[NS * (BM + BN) * BK];
-
-  int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2, wq = wave & 3;
-  const int wm = grp, wn = wq;
-
-  // Group g transfers A rows and W rows [128 g, 128 g + 128): 8 blocks of 64
-  // slots each; wave wq of the group takes blocks wq and wq + 4.
-  uint32_t voff[TPS], loff[TPS];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int blk = grp * 8 + j * 4 + wq;
-    const int p = blk * 64 + lane, r = p >> 2;
-    const int c = (swz<BK>(r, p & 3) & 31) >> 3;
-    voff[j] = (uint32_t)(((long)min(m0 + r, M - 1) * lda + c * 8) * 2);
-    voff[2 + j] = (uint32_t)(((long)min(n0 + r, N - 1) * ldw + c * 8) * 2);
-    loff[j] = blk * 1024;
-    loff[2 + j] = A_BYTES + blk * 1024;
-  }
-  const uint32_t lds0 = lds_byte_addr(smem);
-  const int nk = K / BK;
-  auto issue = [&](int step, int stage) {
-    const long kb = (long)min(step, nk - 1) * BK * 2;
-    const uint32_t base = lds0 + stage * STAGE_BYTES;
-#pragma unroll
-    for (int q = 0; q < TPS; ++q)
-      dma_1k(base + loff[q], voff[q], (const char*)(q < 2 ? A : W) + kb);
-  };
-
-#pragma unroll
-  for (int st = 0; st < D; ++st) issue(st, st);
-  wait_vmcnt<TPS * (D - 1)>();  // step 0 landed (this wave)
-  __builtin_amdgcn_s_barrier();
-  if (grp == 1) __builtin_amdgcn_s_barrier();  // group 1 runs one phase behind
-
-  f32x16 acc[MI][NI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-
-  GemmFrag<MI, NI> f0, f1;
-  int cur = 0, fill = D % NS;
-  for (int kt = 0; kt < nk; ++kt) {
-    // memory phase: this step's fragments, a later step's transfers
-    const bf16* As = smem + cur * (STAGE_BYTES / 2);
-    __builtin_amdgcn_sched_barrier(0);
-    gemm_frag_load<BK, MI, NI, WTM, WTN>(f0, As, As + BM * BK, wm, wn, 0);
-    issue(kt + D, fill);
-    gemm_frag_load<BK, MI, NI, WTM, WTN>(f1, As, As + BM * BK, wm, wn, 1);
-    if (grp == 1) wait_vmcnt<TPS * (D - 1)>();  // own transfers of step kt+1
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    // compute phase
-    __builtin_amdgcn_s_setprio(1);
-    gemm_frag_mma<MI, NI>(f0, acc);
-    gemm_frag_mma<MI, NI>(f1, acc);
-    __builtin_amdgcn_s_setprio(0);
-    if (grp == 0) wait_vmcnt<TPS * (D - 1)>();  // own transfers of step kt+1
-    __builtin_amdgcn_sched_barrier(0);
-    __builtin_amdgcn_s_barrier();
-    cur = cur + 1 == NS ? 0 : cur + 1;
-    fill = fill + 1 == NS ? 0 : fill + 1;
-  }
-  if (grp == 0) __builtin_amdgcn_s_barrier();
-  wait_vmcnt<0>();  // no transfer may still target this workgroup's LDS
 
   gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
@@ -1056,280 +792,6 @@ __global__ __launch_bounds__(512, 1) void gemm_bf16_pp64p_kernel(
     if (next < ntiles) offsets(next, gnxt);
   }
   if (grp == 0) __builtin_amdgcn_s_barrier();
-}
-
-// ------------------------------------------------------------------ bf16 MFMA GEMM, 3-stage LDS ring
-//
-// As gemm_bf16_kernel (BK = 32), but with three LDS stages: the operands of
-// step k are written to LDS during step k-2, so when step k-1 ends its
-// fragments are already published and the first k-slice of step k is read
-// before step k-1's barrier -- no wave waits for LDS right after a barrier.
-// Global loads still run one step ahead of the LDS writes (two register sets).
-
-template <int BM, int BN, int MI, int NI, int WTM, int WTN>
-__device__ __forceinline__ void gemm_r3_frag(GemmFrag<MI, NI>& f, const bf16* As, const bf16* Ws,
-                                             int wm, int wn, int ks) {
-  gemm_frag_load<32, MI, NI, WTM, WTN>(f, As, Ws, wm, wn, ks);
-}
-
-template <int TAG, int BM, int BN, int WGM, int WGN, int OCC, class Epi>
-__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_r3_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
-  constexpr int BK = 32, KS = 2, CPR = 4;
-  constexpr int NT = 64 * WGM * WGN;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
-  constexpr int MI = WTM / 32, NI = WTN / 32;
-  constexpr int A_CH = BM * CPR / NT, W_CH = BN * CPR / NT;
-  static_assert(A_CH >= 1 && W_CH >= 1 && A_CH * NT == BM * CPR && W_CH * NT == BN * CPR,
-                "tile does not split evenly over the threads");
-  constexpr int AS = BM * BK, WS = BN * BK;  // elements per stage
-  __shared__ __attribute__((aligned(16))) bf16 As[3 * AS];
-  __shared__ __attribute__((aligned(16))) bf16 Ws[3 * WS];
-
-  int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-
-  const bf16* a_src[A_CH];
-  const bf16* w_src[W_CH];
-  int a_off[A_CH], w_off[W_CH];
-#pragma unroll
-  for (int i = 0; i < A_CH; ++i) {
-    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
-    a_src[i] = A + (long)min(m0 + r, M - 1) * lda + c * 8;
-    a_off[i] = swz<BK>(r, c);
-  }
-#pragma unroll
-  for (int i = 0; i < W_CH; ++i) {
-    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
-    w_src[i] = W + (long)min(n0 + r, N - 1) * ldw + c * 8;
-    w_off[i] = swz<BK>(r, c);
-  }
-  const int nk = K / BK;  // even, >= 2
-  const int klast = (nk - 1) * BK;
-
-  GemmRegs<A_CH> ra0, ra1;
-  GemmRegs<W_CH> rw0, rw1;
-  // prologue: steps 0 and 1 into LDS stages 0 and 1, step 2 in register set 0
-  gemm_gload(ra0, a_src, 0);
-  gemm_gload(rw0, w_src, 0);
-  gemm_gload(ra1, a_src, BK);
-  gemm_gload(rw1, w_src, BK);
-  gemm_lstore(ra0, As, a_off);
-  gemm_lstore(rw0, Ws, w_off);
-  gemm_gload(ra0, a_src, min(2 * BK, klast));
-  gemm_gload(rw0, w_src, min(2 * BK, klast));
-  gemm_lstore(ra1, As + AS, a_off);
-  gemm_lstore(rw1, Ws + WS, w_off);
-  __syncthreads();
-
-  f32x16 acc[MI][NI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-
-  GemmFrag<MI, NI> f0, f1;
-  gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f0, As, Ws, wm, wn, 0);
-
-  // step kt: compute LDS stage s (= kt mod 3); the register set holding step
-  // kt+2 goes to stage (kt+2) mod 3; the other set is refilled with step kt+3.
-  auto step = [&](int kt, int s, GemmRegs<A_CH>& ra_w, GemmRegs<W_CH>& rw_w,
-                  GemmRegs<A_CH>& ra_l, GemmRegs<W_CH>& rw_l) {
-    const int kn = min((kt + 3) * BK, klast);
-    gemm_gload(ra_l, a_src, kn);
-    gemm_gload(rw_l, w_src, kn);
-    __builtin_amdgcn_sched_barrier(0);
-    const int s1 = (s == 2) ? 0 : s + 1, s2 = (s1 == 2) ? 0 : s1 + 1;
-    const bf16* as = As + s * AS;
-    const bf16* ws = Ws + s * WS;
-    // k-slice 0 (fragments f0 were read earlier), prefetch slice 1
-    gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f1, as, ws, wm, wn, 1);
-    gemm_frag_mma<MI, NI>(f0, acc);
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i)
-      if (i % 2 == 0) *(u32x4*)(As + s2 * AS + a_off[i]) = ra_w.v[i];
-#pragma unroll
-    for (int i = 0; i < W_CH; ++i)
-      if (i % 2 == 0) *(u32x4*)(Ws + s2 * WS + w_off[i]) = rw_w.v[i];
-    __builtin_amdgcn_sched_barrier(0);
-    // k-slice 1; prefetch slice 0 of the next step (its stage is already published)
-    gemm_r3_frag<BM, BN, MI, NI, WTM, WTN>(f0, As + s1 * AS, Ws + s1 * WS, wm, wn, 0);
-    gemm_frag_mma<MI, NI>(f1, acc);
-#pragma unroll
-    for (int i = 0; i < A_CH; ++i)
-      if (i % 2 == 1) *(u32x4*)(As + s2 * AS + a_off[i]) = ra_w.v[i];
-#pragma unroll
-    for (int i = 0; i < W_CH; ++i)
-      if (i % 2 == 1) *(u32x4*)(Ws + s2 * WS + w_off[i]) = rw_w.v[i];
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
-  };
-
-  int s = 0;
-  for (int kt = 0; kt < nk; kt += 2) {
-    step(kt, s, ra0, rw0, ra1, rw1);  // writes step kt+2 (set 0), loads step kt+3 (set 1)
-    s = (s == 2) ? 0 : s + 1;
-    step(kt + 1, s, ra1, rw1, ra0, rw0);  // writes step kt+3 (set 1), loads step kt+4 (set 0)
-    s = (s == 2) ? 0 : s + 1;
-  }
-
-  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
-}
-
-// ------------------------------------------------------------------ bf16 MFMA GEMM, W in registers
-//
-// Same contract as gemm_bf16_kernel, but W comes pre-shuffled into the MFMA
-// operand order (see preshuffle_kernel): the fragment of 32 W rows x 16 k
-// that a wave feeds to one 32x32x16 MFMA is one contiguous kilobyte, so each
-// wave streams its W fragments from global memory straight into registers
-// with fully coalesced loads, and only A goes through LDS.  That removes the
-// W half of the LDS traffic, the bound of the LDS-staged kernel (LDS reads
-// 128 bytes per clock per CU).  A fragment register is reloaded with the
-// step two ahead right after the MFMAs that consume it.
-
-// W[N][K] -> Wp: chunk (nb, kb, lane) = W[32 nb + lane % 32][16 kb + 8 (lane / 32) .. +7];
-// the chunk index is (nb * (K/16) + kb) * 64 + lane.  Fused-row permutations
-// are applied on the way: row n of the fused matrix is src[n] (a row pointer).
-__global__ __launch_bounds__(256) void preshuffle_kernel(bf16* __restrict__ dst,
-                                                         const bf16* const* __restrict__ src,
-                                                         int N, int K) {
-  const long q = (long)blockIdx.x * 256 + threadIdx.x;
-  const int KB = K / 16;
-  if (q >= (long)(N / 32) * KB * 64) return;  // N*K/8 chunks of 8 elements
-  const int lane = (int)(q & 63);
-  const long blk = q >> 6;
-  const int kb = (int)(blk % KB), nb = (int)(blk / KB);
-  const int n = nb * 32 + (lane & 31), k = kb * 16 + (lane >> 5) * 8;
-  *(u32x4*)(dst + q * 8) = *(const u32x4*)(src[n] + k);
-}
-
-// Row-major assembly with the same row table: dst row n = src[n] (K elements).
-__global__ __launch_bounds__(256) void gather_rows_ptr_kernel(bf16* __restrict__ dst,
-                                                              const bf16* const* __restrict__ src,
-                                                              int N, int K) {
-  const long q = (long)blockIdx.x * 256 + threadIdx.x;  // 16-byte chunk index
-  const int cpr = K / 8;
-  if (q >= (long)N * cpr) return;
-  const int n = (int)(q / cpr), c = (int)(q % cpr);
-  *(u32x4*)(dst + q * 8) = *(const u32x4*)(src[n] + c * 8);
-}
-
-template <int KS, int NI>
-struct WFrag {
-  bf16x8 b[KS][NI];
-};
-
-template <int TAG, int BM, int BN, int WGM, int WGN, int BK, int OCC, class Epi>
-__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_wd_kernel(
-    const bf16* __restrict__ A, int lda, const bf16* __restrict__ Wp, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
-  constexpr int NT = 64 * WGM * WGN;
-  constexpr int WTM = BM / WGM, WTN = BN / WGN;
-  static_assert(WTN % 64 == 0, "wave tile width must be a multiple of 64");
-  constexpr int MI = WTM / 32, NI = WTN / 32, KS = BK / 16;
-  constexpr int CPR = BK / 8;
-  constexpr int A_CH = BM * CPR / NT;
-  static_assert(A_CH >= 1 && A_CH * NT == BM * CPR, "A tile does not split evenly");
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
-
-  int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WGN, wn = wave % WGN;
-  const int lr = lane & 31, lh = lane >> 5;
-
-  const bf16* a_src[A_CH];
-  int a_off[A_CH];
-#pragma unroll
-  for (int i = 0; i < A_CH; ++i) {
-    const int ch = tid + NT * i, r = ch / CPR, c = ch % CPR;
-    a_src[i] = A + (long)min(m0 + r, M - 1) * lda + c * 8;
-    a_off[i] = swz<BK>(r, c);
-  }
-  const int KB = K / 16, NB = N / 32;
-  const bf16* w_src[NI];
-#pragma unroll
-  for (int ni = 0; ni < NI; ++ni) {
-    const int nb = min((n0 + wn * WTN) / 32 + ni, NB - 1);
-    w_src[ni] = Wp + ((long)nb * KB * 64 + lane) * 8;
-  }
-  const int nk = K / BK;  // even, >= 2
-  auto wload = [&](WFrag<KS, NI>& f, int ks, int kt) {
-    const int kb = min(kt, nk - 1) * KS + ks;
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni) f.b[ks][ni] = as_bf16x8(*(const u32x4*)(w_src[ni] + (long)kb * 512));
-  };
-  const int klast = (nk - 1) * BK;
-
-  GemmRegs<A_CH> ra0, ra1;
-  WFrag<KS, NI> wf0, wf1;
-  gemm_gload(ra0, a_src, 0);
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) wload(wf0, ks, 0);
-  gemm_gload(ra1, a_src, BK);
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) wload(wf1, ks, 1);
-  gemm_lstore(ra0, As[0], a_off);
-  __syncthreads();
-
-  f32x16 acc[MI][NI];
-#pragma unroll
-  for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-
-  // one stage: MFMAs of A (LDS stage `as`) x W fragments wf (step kt); wf is
-  // refilled with step kt+2; the other A register set goes to the other stage
-  auto stage = [&](const bf16* as, WFrag<KS, NI>& wf, int kt, const GemmRegs<A_CH>& ra_nx,
-                   bf16* as_nx) {
-    bf16x8 af[2][MI];
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      af[0][mi] = as_bf16x8(*(const u32x4*)(as + swz<BK>(wm * WTM + mi * 32 + lr, lh)));
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks + 1 < KS) {
-#pragma unroll
-        for (int mi = 0; mi < MI; ++mi)
-          af[(ks + 1) & 1][mi] =
-              as_bf16x8(*(const u32x4*)(as + swz<BK>(wm * WTM + mi * 32 + lr, 2 * (ks + 1) + lh)));
-      }
-#pragma unroll
-      for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < NI; ++ni)
-          acc[mi][ni] = mfma32x32x16(af[ks & 1][mi], wf.b[ks][ni], acc[mi][ni]);
-      wload(wf, ks, kt + 2);
-#pragma unroll
-      for (int i = 0; i < A_CH; ++i)
-        if (i % KS == ks) *(u32x4*)(as_nx + a_off[i]) = ra_nx.v[i];
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  for (int kt = 0; kt < nk; kt += 2) {
-    const int k2 = min((kt + 2) * BK, klast), k3 = min((kt + 3) * BK, klast);
-    gemm_gload(ra0, a_src, k2);
-    __builtin_amdgcn_sched_barrier(0);
-    stage(As[0], wf0, kt, ra1, As[1]);
-    __syncthreads();
-    gemm_gload(ra1, a_src, k3);
-    __builtin_amdgcn_sched_barrier(0);
-    stage(As[1], wf1, kt + 1, ra0, As[0]);
-    __syncthreads();
-  }
-
-  gemm_store_tile<MI, NI>(epi, acc, m0 + wm * WTM, n0 + wn * WTN, M, N);
 }
 
 // ------------------------------------------------------------------ fp32 FMA GEMM

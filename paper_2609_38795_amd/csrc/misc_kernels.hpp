@@ -91,6 +91,18 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
     norm4(o + c, *(const f32x4*)(xr + c), g + c, inv);
 }
 
+// Row-major assembly from a table of source rows: dst row n = src[n] (K bf16
+// elements, K a multiple of 8); used to build the fused weight matrices.
+__global__ __launch_bounds__(256) void gather_rows_ptr_kernel(bf16* __restrict__ dst,
+                                                              const bf16* const* __restrict__ src,
+                                                              int N, int K) {
+  const long q = (long)blockIdx.x * 256 + threadIdx.x;  // 16-byte chunk index
+  const int cpr = K / 8;
+  if (q >= (long)N * cpr) return;
+  const int n = (int)(q / cpr), c = (int)(q % cpr);
+  *(u32x4*)(dst + q * 8) = *(const u32x4*)(src[n] + c * 8);
+}
+
 // dst[r, :] = src[idx[r], :]  (row_elems elements of T)
 template <typename T>
 __global__ __launch_bounds__(256) void gather_rows_kernel(T* __restrict__ dst,

@@ -382,42 +382,16 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     }
     if (cfg == 0)
       cfg = tiles(256, 256) >= 256 ? ((K % 64) == 0 ? 19 : 4) : (tiles(128, 128) >= 256 ? 2 : 3);
-    // the direct-to-LDS kernels address operands with 32-bit byte offsets
-    const bool dma_ok = (K % 32) == 0 && ((size_t)(M - 1) * lda + K) * 2 <= 0xFFFFFFFFull &&
-                        ((size_t)(N - 1) * ldw + K) * 2 <= 0xFFFFFFFFull;
-    if (cfg >= 11 && cfg <= 16 && !dma_ok) cfg = 4;
     if ((cfg == 17 || cfg == 19) && (K % 64) != 0) cfg = 4;
     const bool k64 = (K % 128) == 0;
-    const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg == 6 || cfg == 8 || cfg == 9 ||
-                    (cfg >= 11 && cfg <= 13) || cfg >= 15)
-                       ? 256
-                       : (cfg == 3 ? 64 : 128);
-    const int bn = (cfg == 4 || cfg == 5 || cfg == 6 || cfg == 9 || (cfg >= 11 && cfg <= 13) || cfg >= 15) ? 256 : 128;
+    const int bm = (cfg == 1 || cfg == 4 || cfg == 5 || cfg >= 17) ? 256 : (cfg == 3 ? 64 : 128);
+    const int bn = (cfg == 4 || cfg == 5 || cfg >= 17) ? 256 : 128;
     const int tm = (M + bm - 1) / bm, tn = (N + bn - 1) / bn;
     const int nb = tm * tn;
 #define ALR_GEMM(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                      \
   gemm_bf16_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                          \
       <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
-#define ALR_GEMM_R3(BM_, BN_, WGM_, WGN_, OCC_)                                        \
-  gemm_bf16_r3_kernel<TAG, BM_, BN_, WGM_, WGN_, OCC_, Epi>                            \
-      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
-#define ALR_GEMM_WD(BM_, BN_, WGM_, WGN_, BK_, OCC_)                                   \
-  gemm_bf16_wd_kernel<TAG, BM_, BN_, WGM_, WGN_, BK_, OCC_, Epi>                       \
-      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, M, N, K, tm, tn, epi)
-#define ALR_GEMM_DMA(BM_, BN_, WGM_, WGN_, NS_, OCC_)                                  \
-  gemm_bf16_dma_kernel<TAG, BM_, BN_, WGM_, WGN_, NS_, OCC_, Epi>                      \
-      <<<nb, 64 * WGM_ * WGN_, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi)
     switch (cfg) {
-      case 11: ALR_GEMM_DMA(256, 256, 2, 4, 4, 1); break;
-      case 12: ALR_GEMM_DMA(256, 256, 2, 4, 5, 1); break;
-      case 13: ALR_GEMM_DMA(256, 256, 2, 2, 4, 1); break;
-      case 14: ALR_GEMM_DMA(128, 128, 2, 2, 4, 2); break;
-      case 15:
-        gemm_bf16_pp_kernel<TAG, 4, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
-        break;
-      case 16:
-        gemm_bf16_pp_kernel<TAG, 5, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
-        break;
       case 17:
         gemm_bf16_pp64_kernel<TAG, Epi><<<nb, 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
         break;
@@ -425,11 +399,6 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         gemm_bf16_pp64p_kernel<TAG, Epi>
             <<<std::min(nb, ctx->n_cu), 512, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
         break;
-      case 9: ALR_GEMM_R3(256, 256, 2, 4, 1); break;
-      case 10: ALR_GEMM_R3(128, 128, 2, 2, 2); break;
-      case 6: ALR_GEMM_WD(256, 256, 2, 4, 32, 1); break;
-      case 7: ALR_GEMM_WD(128, 128, 2, 2, 32, 2); break;
-      case 8: ALR_GEMM_WD(256, 128, 2, 2, 32, 1); break;
       case 5: if (k64) ALR_GEMM(256, 256, 2, 2, 64, 1); else ALR_GEMM(256, 256, 2, 2, 32, 1); break;
       case 4: if (k64) ALR_GEMM(256, 256, 2, 4, 64, 1); else ALR_GEMM(256, 256, 2, 4, 32, 1); break;
       case 1: if (k64) ALR_GEMM(256, 128, 2, 2, 64, 1); else ALR_GEMM(256, 128, 2, 2, 32, 1); break;
@@ -437,9 +406,6 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
       default: if (k64) ALR_GEMM(64, 128, 2, 2, 64, 2); else ALR_GEMM(64, 128, 2, 2, 32, 4); break;
     }
 #undef ALR_GEMM
-#undef ALR_GEMM_R3
-#undef ALR_GEMM_WD
-#undef ALR_GEMM_DMA
   } else {
     const int tm = (M + GF_M - 1) / GF_M, tn = (N + GF_N - 1) / GF_N;
     gemm_f32_kernel<TAG, Epi><<<tm * tn, 256, 0, st>>>(A, lda, W, ldw, M, N, K, tm, tn, epi);
@@ -1343,7 +1309,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || tile > 19) return ALR_E_INVALID_ARG;
+  if (tile < 0 || (tile > 5 && tile < 17) || tile > 19) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
@@ -1352,21 +1318,6 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   alr_ctx dummy;
   if (dtype == ALR_BF16) {
     const bf16* Wk = (const bf16*)W;
-    if (tile >= 6 && tile <= 8) {
-      // the W-from-registers kernel reads W pre-shuffled: shuffle into the scratch buffer
-      const size_t wbytes = (size_t)N * K * 2, need = wbytes + (size_t)N * sizeof(void*);
-      if (!scratch || scratch_bytes < need) return ALR_E_WORKSPACE;
-      std::vector<const bf16*> rp(N);
-      for (int n = 0; n < N; ++n) rp[n] = Wk + (size_t)n * K;
-      const bf16** drp = reinterpret_cast<const bf16**>(static_cast<char*>(scratch) + wbytes);
-      if (hipMemcpyAsync(drp, rp.data(), N * sizeof(void*), hipMemcpyHostToDevice, s) != hipSuccess)
-        return ALR_E_HIP;
-      const long chunks = (long)(N / 32) * (K / 16) * 64;  // N*K/8
-      preshuffle_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
-          static_cast<bf16*>(scratch), drp, N, K);
-      if (hipStreamSynchronize(s) != hipSuccess) return ALR_E_HIP;
-      Wk = static_cast<const bf16*>(scratch);
-    }
     if (tile == 18) {  // split-K: partial sums in the scratch buffer
       if (!scratch || scratch_bytes < (size_t)2 * M * N * 4) return ALR_E_WORKSPACE;
       dummy.splitk_buf = static_cast<float*>(scratch);

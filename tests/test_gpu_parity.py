@@ -20,11 +20,8 @@ def _print(*a):
 
 # ------------------------------------------------------------------ GEMM kernels
 @pytest.mark.parametrize("dtype,tile", [("bf16", 0), ("f32", 0), ("bf16", 1), ("bf16", 2),
-                                        ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 6),
-                                        ("bf16", 7), ("bf16", 8), ("bf16", 9), ("bf16", 10),
-                                        ("bf16", 11), ("bf16", 12), ("bf16", 13), ("bf16", 14),
-                                        ("bf16", 15), ("bf16", 16), ("bf16", 17), ("bf16", 18),
-                                        ("bf16", 19)])
+                                        ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 17),
+                                        ("bf16", 18), ("bf16", 19)])
 @pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 192, 256), (1024, 640, 1152)])
 def test_gemm_kernel(dtype, tile, M, N, K):
     """Every GEMM kernel variant against a float64 product, ragged M and partial N tiles."""
