@@ -120,9 +120,10 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 constexpr int AT_KT = 64;
 // Decode split: the shared keys of every (anchor group, kv head) are cut into
 // chunks of a common number ct of 64-key tiles.  The host picks ct to
-// minimise (rounds of workgroups) x (ct + AT_DECODE_ITEM_OVERHEAD), with two
-// workgroups per CU, among the ct that give at most AT_DECODE_MAX_ITEMS items
-// and never fewer than AT_DECODE_MIN_TILES tiles per item.
+// minimise the simulated makespan (list scheduling, largest item first, two
+// workgroups per CU, an item costing its tiles + AT_DECODE_ITEM_OVERHEAD)
+// among the ct that give at most AT_DECODE_MAX_ITEMS items and never fewer
+// than AT_DECODE_MIN_TILES tiles per item.
 constexpr int AT_DECODE_MAX_ITEMS = 2048;
 constexpr int AT_DECODE_ITEM_OVERHEAD = 3;  // prologue, partial store and merge, in tiles
 constexpr int AT_DECODE_MIN_TILES = 4;
@@ -246,9 +247,13 @@ __device__ __forceinline__ void attn_tile_update(const AttnTile<HD>& t, const bf
       tmax = fmaxf(tmax, s[kb][r]);
     }
   tmax = max_xor32(tmax);
-  const float m_new = fmaxf(m, tmax);
+  // The reference m moves only when the tile's max exceeds it by more than 8
+  // in the exponent (or on the first keys): the weights exp2(s - m) then stay
+  // below 256 and the accumulators are rescaled on few tiles, not on every
+  // tile whose max grew.  o, l and m stay consistent, so o / l is unchanged.
+  const bool grew = tmax * scale_log2 > m * scale_log2 + 8.f;
+  const float m_new = grew ? tmax : m;
   const float mref = (m_new == -INFINITY) ? 0.f : m_new * scale_log2;
-  const bool grew = m_new > m;
   const float alpha = grew ? fast_exp2(m * scale_log2 - mref) : 1.f;
   float psum = 0.f;
 #pragma unroll

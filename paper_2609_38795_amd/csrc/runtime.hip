@@ -347,8 +347,7 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
   if constexpr (std::is_same<T, bf16>::value) {
     // W row-major.  256x256 ping-pong (BK = 64), persistent over the tiles, for
     // the prefill and wide decode GEMMs, 128x128 (then 64x128) LDS-staged tiles
-    // where 256x256 would leave CUs idle.  force_tile (debug hook only) picks any variant; 6..8 need W
-    // pre-shuffled.
+    // where 256x256 would leave CUs idle.  force_tile (debug hook only) picks any variant.
     auto tiles = [&](int bm, int bn) { return ((M + bm - 1) / bm) * ((N + bn - 1) / bn); };
     int cfg = force_tile;
     // Split-K over the 256x256 ping-pong kernel when its tiles leave CUs idle:
@@ -1081,8 +1080,12 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
       // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
       // at absolute key positions, so the groups of one sequence read the same
       // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
-      // dealt so that consecutive items run on one XCD (workgroup b is
-      // dispatched to XCD b % 8): the groups sharing a chunk meet in that L2.
+      // dealt in contiguous runs to the XCDs (workgroup b is dispatched to XCD
+      // b % 8), so the groups sharing a chunk meet in that XCD's L2; within an
+      // XCD the items go largest first (stable), so the short tail chunks fill
+      // the slots the long ones leave.  ct minimises the makespan of that
+      // order under list scheduling on the XCD's 2 * CUs / 8 workgroup slots,
+      // an item costing its tiles + AT_DECODE_ITEM_OVERHEAD.
       const int ag = anchor_group(c), G = c.n_kv_heads;
       struct Grp {
         int f, cnt, sq, a_max, ntile;
@@ -1105,15 +1108,59 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
       for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
       const int ct_min = (int)std::max<long>(
           AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
-      const long slots = 2L * ctx->n_cu;
+      // logical item list for chunk length ct: (group index, chunk)
+      auto list_items = [&](int ct, std::vector<std::pair<int, int>>& out, std::vector<int>& kvh) {
+        out.clear();
+        kvh.clear();
+        for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
+          size_t g1 = g0;
+          int max_chunks = 0;
+          while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
+            max_chunks = std::max(max_chunks, (gs[g1].ntile + ct - 1) / ct);
+            ++g1;
+          }
+          for (int g = 0; g < G; ++g)
+            for (int ch = 0; ch < max_chunks; ++ch)
+              for (size_t gi = g0; gi < g1; ++gi)
+                if (ch < (gs[gi].ntile + ct - 1) / ct) {
+                  out.emplace_back((int)gi, ch);
+                  kvh.push_back(g);
+                }
+          g0 = g1;
+        }
+      };
+      auto item_tiles = [&](int ct, const std::pair<int, int>& it) {
+        return std::min(ct, gs[it.first].ntile - it.second * ct);
+      };
+      // XCD x runs logical items [x * per, (x + 1) * per), largest first
+      auto xcd_order = [&](int ct, const std::vector<std::pair<int, int>>& lg, size_t per, int x) {
+        std::vector<int> idx;
+        for (size_t li = (size_t)x * per; li < std::min(lg.size(), (size_t)(x + 1) * per); ++li)
+          idx.push_back((int)li);
+        std::stable_sort(idx.begin(), idx.end(), [&](int u, int v) {
+          return item_tiles(ct, lg[u]) > item_tiles(ct, lg[v]);
+        });
+        return idx;
+      };
+      const int xslots = std::max(1, 2 * ctx->n_cu / 8);
+      std::vector<std::pair<int, int>> lg;
+      std::vector<int> lg_kvh;
       int ct = std::max(ct_min, max_nt);
-      double best = -1.0;
+      long best = -1;
       for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
-        long items = 0;
-        for (const Grp& gr : gs) items += (long)((gr.ntile + cand - 1) / cand) * G;
-        const double cost = (double)((items + slots - 1) / slots) * (cand + AT_DECODE_ITEM_OVERHEAD);
-        if (best < 0 || cost < best) {
-          best = cost;
+        list_items(cand, lg, lg_kvh);
+        const size_t per = (lg.size() + 7) / 8;
+        long span = 0;
+        for (int x = 0; x < 8; ++x) {
+          std::vector<long> slot(xslots, 0);  // busy-until per slot
+          for (int li : xcd_order(cand, lg, per, x)) {
+            auto it = std::min_element(slot.begin(), slot.end());
+            *it += item_tiles(cand, lg[li]) + AT_DECODE_ITEM_OVERHEAD;
+          }
+          span = std::max(span, *std::max_element(slot.begin(), slot.end()));
+        }
+        if (best < 0 || span < best) {
+          best = span;
           ct = cand;
         }
       }
@@ -1124,32 +1171,20 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
         for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) ctx->h_grprow[rr] = (int)gi;
         part += nchunk * G;
       }
-      std::vector<DecodeItem> logical;
-      for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
-        size_t g1 = g0;
-        int max_chunks = 0;
-        while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
-          max_chunks = std::max(max_chunks, ctx->h_groups[g1].nchunk);
-          ++g1;
-        }
-        const int sq = gs[g0].sq;
-        for (int g = 0; g < G; ++g)
-          for (int ch = 0; ch < max_chunks; ++ch)
-            for (size_t gi = g0; gi < g1; ++gi) {
-              const DecodeGroup& dg = ctx->h_groups[gi];
-              if (ch >= dg.nchunk) continue;
-              const int kb = ch * ct * AT_KT;
-              const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
-              logical.push_back(DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[sq],
-                                           ctx->seq_vcol[sq], kb, ke, dg.part0 + g * dg.nchunk + ch});
-            }
-        g0 = g1;
-      }
-      const size_t per = (logical.size() + 7) / 8;
+      list_items(ct, lg, lg_kvh);
+      const size_t per = (lg.size() + 7) / 8;
       ctx->h_dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
-      for (size_t b = 0; b < per * 8; ++b) {
-        const size_t li = (b % 8) * per + b / 8;
-        if (li < logical.size()) ctx->h_dwork[b] = logical[li];
+      for (int x = 0; x < 8; ++x) {
+        const std::vector<int> idx = xcd_order(ct, lg, per, x);
+        for (size_t i = 0; i < idx.size(); ++i) {
+          const int gi = lg[idx[i]].first, ch = lg[idx[i]].second, g = lg_kvh[idx[i]];
+          const DecodeGroup& dg = ctx->h_groups[gi];
+          const int kb = ch * ct * AT_KT;
+          const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
+          ctx->h_dwork[x + 8 * i] = DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[gs[gi].sq],
+                                               ctx->seq_vcol[gs[gi].sq], kb, ke,
+                                               dg.part0 + g * dg.nchunk + ch};
+        }
       }
     }
   }
