@@ -106,6 +106,30 @@ def test_small_bf16_workload_subset():
     assert rep.ok()
 
 
+@pytest.mark.parametrize("dtype,hd,H,G", [("bf16", 128, 8, 2), ("bf16", 64, 8, 2), ("f32", 32, 4, 2)])
+def test_ragged_sequences_and_edge_anchors(dtype, hd, H, G):
+    """One prefill over sequences of ragged lengths (300, 129, 64 and 1 tokens: partial key tiles,
+    a one-token prefix); anchors at each sequence's first and last position, one anchor twice, and
+    rollout positions past the sequence end."""
+    lens = [300, 129, 64, 1]
+    base = W.get("small_bf16")
+    w = W.scaled(base, f"ragged_{dtype}_{hd}", n_layers=2, d_model=256, n_heads=H, n_kv_heads=G,
+                 head_dim=hd, d_ffn=512, vocab=2048, feat_layers=(0, 1), dtype=dtype,
+                 n_seq=len(lens), seq_len=max(lens), block=5)
+    tok_pad = W.random_tokens(2048, (len(lens), max(lens)), 17 + hd, dist="zipf")
+    a_seq = np.array([0, 0, 0, 1, 1, 1, 2, 2, 3, 1], np.int32)
+    a_pos = np.array([0, 299, 150, 0, 128, 128, 63, 31, 0, 64], np.int32)
+    inp = W.Inputs(w, W.random_weights(w.shape, 31 + hd, scale=0.05, norm_gain="random"),
+                   tok_pad, a_seq, a_pos, None, None)
+    eng = make_engine(inp, max_anchors=len(a_seq), max_block=w.block)
+    flat = np.concatenate([tok_pad[s, :n] for s, n in enumerate(lens)]).astype(np.int32)
+    eng.prefill(torch.from_numpy(flat).to(eng.device), lens)
+    rep = compare(inp, w.shape, np.arange(len(a_seq)), runner(eng, a_seq, a_pos, w.block), w.block)
+    eng.close()
+    _print(rep)
+    assert rep.ok()
+
+
 # ------------------------------------------------------------------ invariants (bit-exact)
 def test_permutation_duplicates_and_slot0():
     inp = W.make_inputs("tiny_fp32")
