@@ -177,6 +177,8 @@ alr_status alr_prefill_positions(alr_ctx* ctx, int32_t n_seq, const int32_t* seq
                                  alr_stream stream);
 
 /* Greedy rollout of `block` slots from every anchor of the last prefill.
+ *   n_anchor   in [1, max_anchors] and block in [1, max_block]; an empty
+ *              request is ALR_E_INVALID_ARG (nothing is launched).
  *   anchor_seq, anchor_pos  HOST int32 [n_anchor]: sequence index and position;
  *              0 <= anchor_pos < seq_len[anchor_seq]; anchor_pos + block - 1 <
  *              max_pos.  Any order; duplicates allowed (identical outputs).

@@ -113,6 +113,9 @@ def test_rollout_checks(lib):
     # too many anchors for the context's limits
     lim_small = binding.make_limits(w.n_tokens, w.n_seq, 8, w.block)
     assert binding.check_rollout(w.shape, w.max_pos, lim_small, seq_len, a_s, a_p, w.block)[0] == 1
+    # an empty request is an argument error, not a silent no-op
+    st, msg = binding.check_rollout(w.shape, w.max_pos, lim, seq_len, a_s[:0], a_p[:0], w.block)
+    assert st == 1 and "n_anchor 0" in msg
 
 
 def test_create_rejects_bad_arguments_without_gpu(lib):
