@@ -18,7 +18,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <functional>
 #include <numeric>
+#include <queue>
 #include <string>
 #include <type_traits>
 #include <vector>
@@ -1152,12 +1154,17 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
         const size_t per = (lg.size() + 7) / 8;
         long span = 0;
         for (int x = 0; x < 8; ++x) {
-          std::vector<long> slot(xslots, 0);  // busy-until per slot
+          // busy-until time of each slot; the next item goes to the earliest
+          std::priority_queue<long, std::vector<long>, std::greater<long>> slot;
+          for (int i = 0; i < xslots; ++i) slot.push(0);
+          long last = 0;
           for (int li : xcd_order(cand, lg, per, x)) {
-            auto it = std::min_element(slot.begin(), slot.end());
-            *it += item_tiles(cand, lg[li]) + AT_DECODE_ITEM_OVERHEAD;
+            const long t = slot.top() + item_tiles(cand, lg[li]) + AT_DECODE_ITEM_OVERHEAD;
+            slot.pop();
+            slot.push(t);
+            last = std::max(last, t);
           }
-          span = std::max(span, *std::max_element(slot.begin(), slot.end()));
+          span = std::max(span, last);
         }
         if (best < 0 || span < best) {
           best = span;
