@@ -37,6 +37,27 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           int32_t N, int32_t K, int32_t tile, void* scratch,
                           size_t scratch_bytes, alr_stream stream);
 
+/* Work plan of the decode attention for a rollout request (host only, no GPU
+ * needed; the same planner alr_rollout runs).  n_seq sequences of lengths
+ * seq_len[] laid out as alr_prefill lays them out (keys of sequence i from the
+ * sum of the earlier lengths; its transposed values from the sum of the
+ * earlier lengths each rounded up to 64), n_anchor anchors as for
+ * alr_check_rollout, a device of n_cu compute units.  Writes the key-chunk
+ * length in 64-key tiles to *ct_out, the simulated makespan (tiles, an item
+ * costing its tiles + 3) to *makespan_out and the number of work items,
+ * padding included, to *n_items_out; if items_out is not NULL, item b (run on
+ * XCD b % 8) as 6 int32 at items_out[6 b]: first anchor in sorted order (by
+ * sequence, then position, then the caller's index), anchor count (0 for
+ * padding), kv head, first key, end key (exclusive), partial-output index.
+ * ALR_E_UNSUPPORTED when the config's attention has no plan (fp32, or a head
+ * size other than 64 and 128), ALR_E_WORKSPACE when the items exceed
+ * max_items, the statuses of alr_check_config / alr_check_rollout otherwise. */
+alr_status alr_debug_decode_plan(const alr_config* cfg, int32_t n_cu, int32_t n_seq,
+                                 const int32_t* seq_len, int32_t n_anchor,
+                                 const int32_t* anchor_seq, const int32_t* anchor_pos,
+                                 int32_t* ct_out, int32_t* makespan_out, int32_t* n_items_out,
+                                 int32_t* items_out, int32_t max_items);
+
 /* Kernel launch sites whose device time can be measured with alr_profile_*. */
 typedef enum {
   ALR_PROF_PREFILL_QKV = 1,   /* prefill QKV GEMM (+RoPE, shared K/V store)        */

@@ -25,7 +25,7 @@ STATUS = {0: "ALR_OK", 1: "ALR_E_INVALID_ARG", 2: "ALR_E_OUT_OF_RANGE", 3: "ALR_
 EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_create",
            "alr_prefill", "alr_prefill_positions", "alr_rollout", "alr_rollout_topk",
            "alr_corpus_labels", "alr_ira_assemble", "alr_slot_weights", "alr_last_error", "alr_status_string", "alr_destroy",
-           "alr_debug_gemm", "alr_profile_start", "alr_profile_stop")
+           "alr_debug_gemm", "alr_debug_decode_plan", "alr_profile_start", "alr_profile_stop")
 ALR_TOPK = 8
 
 
@@ -110,6 +110,9 @@ def load_library() -> ctypes.CDLL:
     lib.alr_destroy.restype = None
     lib.alr_debug_gemm.argtypes = [i32, vp, vp, vp, i32, i32, i32, i32, vp, sz, vp]
     lib.alr_debug_gemm.restype = ctypes.c_int
+    lib.alr_debug_decode_plan.argtypes = [cfgp, i32, i32, i32p, i32, i32p, i32p, i32p, i32p, i32p,
+                                          i32p, i32]
+    lib.alr_debug_decode_plan.restype = ctypes.c_int
     lib.alr_profile_start.argtypes = [vp, i32, i32]
     lib.alr_profile_start.restype = ctypes.c_int
     lib.alr_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
@@ -157,6 +160,25 @@ def check_rollout(shape, max_pos, limits: AlrLimits, seq_len: Sequence[int], anc
     st = lib.alr_check_rollout(ctypes.byref(cfg), ctypes.byref(limits), len(sl), _i32p(sl),
                                len(a_s), _i32p(a_s), _i32p(a_p), block, buf, 256)
     return st, buf.value.decode()
+
+
+def decode_plan(shape, max_pos, n_cu: int, seq_len: Sequence[int], anchor_seq, anchor_pos,
+                max_items: int = 1 << 16):
+    """Host-only decode-attention work plan: (chunk tiles, makespan, items [n, 6] int32 with
+    columns first sorted anchor, anchor count, kv head, first key, end key, partial index)."""
+    lib = load_library()
+    cfg = make_config(shape, max_pos)
+    sl = np.ascontiguousarray(seq_len, dtype=np.int32)
+    a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+    a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+    ct, span, n = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    items = np.zeros((max_items, 6), np.int32)
+    st = lib.alr_debug_decode_plan(ctypes.byref(cfg), n_cu, len(sl), _i32p(sl), len(a_s),
+                                   _i32p(a_s), _i32p(a_p), ctypes.byref(ct), ctypes.byref(span),
+                                   ctypes.byref(n), _i32p(items), max_items)
+    if st != 0:
+        raise AlrError(st, "alr_debug_decode_plan")
+    return ct.value, span.value, items[:n.value].copy()
 
 
 class Engine:

@@ -1034,6 +1034,138 @@ namespace {
 // Validates an anchor request, sorts the anchors by (sequence, position) and
 // uploads the per-anchor tables (and, for a rollout, the decode-attention work
 // split) to the workspace on stream s.
+// Decode attention work plan for n anchors sorted by (sequence, position):
+// seqs[r] and apos[r] are sorted anchor r's sequence and position; seq_off and
+// seq_vcol give each sequence's first K-cache row and first V^T column.
+// Fills the work items (dealt to XCDs: item b runs on XCD b % 8, padding
+// items have count 0), the anchor groups and each sorted anchor's group.
+// Returns the chunk length in 64-key tiles; *makespan receives the simulated
+// makespan in tiles.
+int plan_decode(const alr_config& c, int n_cu, int n, const int* seqs, const int* apos,
+                const int* seq_off, const int* seq_vcol, std::vector<DecodeItem>& dwork,
+                std::vector<DecodeGroup>& groups, std::vector<int>& grprow,
+                long* makespan = nullptr) {
+  dwork.clear();
+  groups.clear();
+  grprow.assign(n, 0);
+  // Groups of up to 128/rep sorted anchors of one sequence.  The shared keys
+  // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
+  // at absolute key positions, so the groups of one sequence read the same
+  // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
+  // dealt in contiguous runs to the XCDs (workgroup b is dispatched to XCD
+  // b % 8), so the groups sharing a chunk meet in that XCD's L2; within an
+  // XCD the items go largest first (stable), so the short tail chunks fill
+  // the slots the long ones leave.  ct minimises the makespan of that
+  // order under list scheduling on the XCD's 2 * CUs / 8 workgroup slots,
+  // an item costing its tiles + AT_DECODE_ITEM_OVERHEAD.
+  const int ag = anchor_group(c), G = c.n_kv_heads;
+  struct Grp {
+    int f, cnt, sq, a_max, ntile;
+  };
+  std::vector<Grp> gs;
+  long total_tiles = 0;
+  for (int r0 = 0; r0 < n;) {
+    const int sq = seqs[r0];
+    int r1 = r0;
+    while (r1 < n && seqs[r1] == sq) ++r1;
+    for (int f = r0; f < r1; f += ag) {
+      const int cnt = std::min(ag, r1 - f);
+      const int a_max = apos[f + cnt - 1];
+      gs.push_back(Grp{f, cnt, sq, a_max, (a_max + AT_KT) / AT_KT});
+      total_tiles += (long)gs.back().ntile * G;
+    }
+    r0 = r1;
+  }
+  int max_nt = 1;
+  for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
+  const int ct_min = (int)std::max<long>(
+      AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
+  // logical item list for chunk length ct: (group index, chunk)
+  auto list_items = [&](int ct, std::vector<std::pair<int, int>>& out, std::vector<int>& kvh) {
+    out.clear();
+    kvh.clear();
+    for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
+      size_t g1 = g0;
+      int max_chunks = 0;
+      while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
+        max_chunks = std::max(max_chunks, (gs[g1].ntile + ct - 1) / ct);
+        ++g1;
+      }
+      for (int g = 0; g < G; ++g)
+        for (int ch = 0; ch < max_chunks; ++ch)
+          for (size_t gi = g0; gi < g1; ++gi)
+            if (ch < (gs[gi].ntile + ct - 1) / ct) {
+              out.emplace_back((int)gi, ch);
+              kvh.push_back(g);
+            }
+      g0 = g1;
+    }
+  };
+  auto item_tiles = [&](int ct, const std::pair<int, int>& it) {
+    return std::min(ct, gs[it.first].ntile - it.second * ct);
+  };
+  // XCD x runs logical items [x * per, (x + 1) * per), largest first
+  auto xcd_order = [&](int ct, const std::vector<std::pair<int, int>>& lg, size_t per, int x) {
+    std::vector<int> idx;
+    for (size_t li = (size_t)x * per; li < std::min(lg.size(), (size_t)(x + 1) * per); ++li)
+      idx.push_back((int)li);
+    std::stable_sort(idx.begin(), idx.end(), [&](int u, int v) {
+      return item_tiles(ct, lg[u]) > item_tiles(ct, lg[v]);
+    });
+    return idx;
+  };
+  const int xslots = std::max(1, 2 * n_cu / 8);
+  std::vector<std::pair<int, int>> lg;
+  std::vector<int> lg_kvh;
+  int ct = std::max(ct_min, max_nt);
+  long best = -1;
+  for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
+    list_items(cand, lg, lg_kvh);
+    const size_t per = (lg.size() + 7) / 8;
+    long span = 0;
+    for (int x = 0; x < 8; ++x) {
+      // busy-until time of each slot; the next item goes to the earliest
+      std::priority_queue<long, std::vector<long>, std::greater<long>> slot;
+      for (int i = 0; i < xslots; ++i) slot.push(0);
+      long last = 0;
+      for (int li : xcd_order(cand, lg, per, x)) {
+        const long t = slot.top() + item_tiles(cand, lg[li]) + AT_DECODE_ITEM_OVERHEAD;
+        slot.pop();
+        slot.push(t);
+        last = std::max(last, t);
+      }
+      span = std::max(span, last);
+    }
+    if (best < 0 || span < best) {
+      best = span;
+      ct = cand;
+    }
+  }
+  int part = 0;
+  for (size_t gi = 0; gi < gs.size(); ++gi) {
+    const int nchunk = (gs[gi].ntile + ct - 1) / ct;
+    groups.push_back(DecodeGroup{gs[gi].f, nchunk, part});
+    for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) grprow[rr] = (int)gi;
+    part += nchunk * G;
+  }
+  list_items(ct, lg, lg_kvh);
+  const size_t per = (lg.size() + 7) / 8;
+  dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
+  for (int x = 0; x < 8; ++x) {
+    const std::vector<int> idx = xcd_order(ct, lg, per, x);
+    for (size_t i = 0; i < idx.size(); ++i) {
+      const int gi = lg[idx[i]].first, ch = lg[idx[i]].second, g = lg_kvh[idx[i]];
+      const DecodeGroup& dg = groups[gi];
+      const int kb = ch * ct * AT_KT;
+      const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
+      dwork[x + 8 * i] = DecodeItem{gs[gi].f, gs[gi].cnt, g, seq_off[gs[gi].sq],
+                                    seq_vcol[gs[gi].sq], kb, ke, dg.part0 + g * dg.nchunk + ch};
+    }
+  }
+  if (makespan) *makespan = best;
+  return ct;
+}
+
 alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
                            const int32_t* anchor_pos, int32_t block, bool rollout,
                            hipStream_t s) {
@@ -1078,121 +1210,10 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
   ctx->h_grprow.assign(n, 0);
   if (rollout) {
     if (mfma_attn(c)) {
-      // Groups of up to 128/rep sorted anchors of one sequence.  The shared keys
-      // 0..a_max of a group are cut, per kv head, into chunks of ct 64-key tiles
-      // at absolute key positions, so the groups of one sequence read the same
-      // chunks.  Work items are listed by (sequence, kv head, chunk, group) and
-      // dealt in contiguous runs to the XCDs (workgroup b is dispatched to XCD
-      // b % 8), so the groups sharing a chunk meet in that XCD's L2; within an
-      // XCD the items go largest first (stable), so the short tail chunks fill
-      // the slots the long ones leave.  ct minimises the makespan of that
-      // order under list scheduling on the XCD's 2 * CUs / 8 workgroup slots,
-      // an item costing its tiles + AT_DECODE_ITEM_OVERHEAD.
-      const int ag = anchor_group(c), G = c.n_kv_heads;
-      struct Grp {
-        int f, cnt, sq, a_max, ntile;
-      };
-      std::vector<Grp> gs;
-      long total_tiles = 0;
-      for (int r0 = 0; r0 < n;) {
-        const int sq = anchor_seq[order[r0]];
-        int r1 = r0;
-        while (r1 < n && anchor_seq[order[r1]] == sq) ++r1;
-        for (int f = r0; f < r1; f += ag) {
-          const int cnt = std::min(ag, r1 - f);
-          const int a_max = apos[f + cnt - 1];
-          gs.push_back(Grp{f, cnt, sq, a_max, (a_max + AT_KT) / AT_KT});
-          total_tiles += (long)gs.back().ntile * G;
-        }
-        r0 = r1;
-      }
-      int max_nt = 1;
-      for (const Grp& gr : gs) max_nt = std::max(max_nt, gr.ntile);
-      const int ct_min = (int)std::max<long>(
-          AT_DECODE_MIN_TILES, (total_tiles + AT_DECODE_MAX_ITEMS - 1) / AT_DECODE_MAX_ITEMS);
-      // logical item list for chunk length ct: (group index, chunk)
-      auto list_items = [&](int ct, std::vector<std::pair<int, int>>& out, std::vector<int>& kvh) {
-        out.clear();
-        kvh.clear();
-        for (size_t g0 = 0; g0 < gs.size();) {  // g0..g1: the groups of one sequence
-          size_t g1 = g0;
-          int max_chunks = 0;
-          while (g1 < gs.size() && gs[g1].sq == gs[g0].sq) {
-            max_chunks = std::max(max_chunks, (gs[g1].ntile + ct - 1) / ct);
-            ++g1;
-          }
-          for (int g = 0; g < G; ++g)
-            for (int ch = 0; ch < max_chunks; ++ch)
-              for (size_t gi = g0; gi < g1; ++gi)
-                if (ch < (gs[gi].ntile + ct - 1) / ct) {
-                  out.emplace_back((int)gi, ch);
-                  kvh.push_back(g);
-                }
-          g0 = g1;
-        }
-      };
-      auto item_tiles = [&](int ct, const std::pair<int, int>& it) {
-        return std::min(ct, gs[it.first].ntile - it.second * ct);
-      };
-      // XCD x runs logical items [x * per, (x + 1) * per), largest first
-      auto xcd_order = [&](int ct, const std::vector<std::pair<int, int>>& lg, size_t per, int x) {
-        std::vector<int> idx;
-        for (size_t li = (size_t)x * per; li < std::min(lg.size(), (size_t)(x + 1) * per); ++li)
-          idx.push_back((int)li);
-        std::stable_sort(idx.begin(), idx.end(), [&](int u, int v) {
-          return item_tiles(ct, lg[u]) > item_tiles(ct, lg[v]);
-        });
-        return idx;
-      };
-      const int xslots = std::max(1, 2 * ctx->n_cu / 8);
-      std::vector<std::pair<int, int>> lg;
-      std::vector<int> lg_kvh;
-      int ct = std::max(ct_min, max_nt);
-      long best = -1;
-      for (int cand = std::max(ct_min, max_nt); cand >= ct_min; --cand) {
-        list_items(cand, lg, lg_kvh);
-        const size_t per = (lg.size() + 7) / 8;
-        long span = 0;
-        for (int x = 0; x < 8; ++x) {
-          // busy-until time of each slot; the next item goes to the earliest
-          std::priority_queue<long, std::vector<long>, std::greater<long>> slot;
-          for (int i = 0; i < xslots; ++i) slot.push(0);
-          long last = 0;
-          for (int li : xcd_order(cand, lg, per, x)) {
-            const long t = slot.top() + item_tiles(cand, lg[li]) + AT_DECODE_ITEM_OVERHEAD;
-            slot.pop();
-            slot.push(t);
-            last = std::max(last, t);
-          }
-          span = std::max(span, last);
-        }
-        if (best < 0 || span < best) {
-          best = span;
-          ct = cand;
-        }
-      }
-      int part = 0;
-      for (size_t gi = 0; gi < gs.size(); ++gi) {
-        const int nchunk = (gs[gi].ntile + ct - 1) / ct;
-        ctx->h_groups.push_back(DecodeGroup{gs[gi].f, nchunk, part});
-        for (int rr = gs[gi].f; rr < gs[gi].f + gs[gi].cnt; ++rr) ctx->h_grprow[rr] = (int)gi;
-        part += nchunk * G;
-      }
-      list_items(ct, lg, lg_kvh);
-      const size_t per = (lg.size() + 7) / 8;
-      ctx->h_dwork.assign(per * 8, DecodeItem{0, 0, 0, 0, 0, 0, 0, 0});
-      for (int x = 0; x < 8; ++x) {
-        const std::vector<int> idx = xcd_order(ct, lg, per, x);
-        for (size_t i = 0; i < idx.size(); ++i) {
-          const int gi = lg[idx[i]].first, ch = lg[idx[i]].second, g = lg_kvh[idx[i]];
-          const DecodeGroup& dg = ctx->h_groups[gi];
-          const int kb = ch * ct * AT_KT;
-          const int ke = std::min(gs[gi].a_max + 1, kb + ct * AT_KT);
-          ctx->h_dwork[x + 8 * i] = DecodeItem{gs[gi].f, gs[gi].cnt, g, ctx->seq_off[gs[gi].sq],
-                                               ctx->seq_vcol[gs[gi].sq], kb, ke,
-                                               dg.part0 + g * dg.nchunk + ch};
-        }
-      }
+      std::vector<int> sq_sorted(n);
+      for (int r = 0; r < n; ++r) sq_sorted[r] = anchor_seq[order[r]];
+      plan_decode(c, ctx->n_cu, n, sq_sorted.data(), apos, ctx->seq_off.data(),
+                  ctx->seq_vcol.data(), ctx->h_dwork, ctx->h_groups, ctx->h_grprow);
     }
   }
   if (ctx->h_dwork.size() > ctx->L.max_dwork || ctx->h_groups.size() > ctx->L.max_groups)
@@ -1345,6 +1366,63 @@ void alr_destroy(alr_ctx* ctx) {
 }
 
 // ------------------------------------------------------------------ debug hooks
+
+alr_status alr_debug_decode_plan(const alr_config* cfg, int32_t n_cu, int32_t n_seq,
+                                 const int32_t* seq_len, int32_t n_anchor,
+                                 const int32_t* anchor_seq, const int32_t* anchor_pos,
+                                 int32_t* ct_out, int32_t* makespan_out, int32_t* n_items_out,
+                                 int32_t* items_out, int32_t max_items) {
+  if (!cfg || !seq_len || !ct_out || !makespan_out || !n_items_out || n_seq <= 0 || n_cu <= 0)
+    return ALR_E_INVALID_ARG;
+  alr_status st = alr_check_config(cfg, nullptr, 0);
+  if (st != ALR_OK) return st;
+  if (!mfma_attn(*cfg)) return ALR_E_UNSUPPORTED;
+  std::vector<int> off(n_seq + 1, 0), vcol(n_seq, 0);
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq_len[i] <= 0) return ALR_E_INVALID_ARG;
+    off[i + 1] = off[i] + seq_len[i];
+    if (i + 1 < n_seq) vcol[i + 1] = vcol[i] + (seq_len[i] + 63) / 64 * 64;
+  }
+  const alr_limits lim{off[n_seq], n_seq, n_anchor, 1};
+  st = check_rollout_impl(*cfg, lim, n_seq, seq_len, n_anchor, anchor_seq, anchor_pos, 1, nullptr,
+                          0);
+  if (st != ALR_OK) return st;
+  const int n = n_anchor;
+  std::vector<int> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  std::sort(order.begin(), order.end(), [&](int x, int y) {
+    if (anchor_seq[x] != anchor_seq[y]) return anchor_seq[x] < anchor_seq[y];
+    if (anchor_pos[x] != anchor_pos[y]) return anchor_pos[x] < anchor_pos[y];
+    return x < y;
+  });
+  std::vector<int> sq(n), ap(n);
+  for (int r = 0; r < n; ++r) {
+    sq[r] = anchor_seq[order[r]];
+    ap[r] = anchor_pos[order[r]];
+  }
+  std::vector<DecodeItem> items;
+  std::vector<DecodeGroup> groups;
+  std::vector<int> grprow;
+  long span = 0;
+  *ct_out = plan_decode(*cfg, n_cu, n, sq.data(), ap.data(), off.data(), vcol.data(), items,
+                        groups, grprow, &span);
+  *makespan_out = (int32_t)span;
+  *n_items_out = (int32_t)items.size();
+  if (items_out) {
+    if ((long)items.size() > max_items) return ALR_E_WORKSPACE;
+    for (size_t b = 0; b < items.size(); ++b) {
+      const DecodeItem& it = items[b];
+      int32_t* o = items_out + 6 * b;
+      o[0] = it.first;
+      o[1] = it.count;
+      o[2] = it.kvh;
+      o[3] = it.kbeg;
+      o[4] = it.kend;
+      o[5] = it.part;
+    }
+  }
+  return ALR_OK;
+}
 
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
                           int32_t N, int32_t K, int32_t tile, void* scratch, size_t scratch_bytes,
