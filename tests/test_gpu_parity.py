@@ -173,6 +173,42 @@ def test_forced_corpus_continuation_matches_later_anchor_slot0():
     eng.close()
 
 
+@pytest.mark.parametrize("dtype,hd", [("bf16", 128), ("f32", 32)])
+def test_second_prefill_replaces_the_first(dtype, hd):
+    """A context reused for a second corpus (other lengths and tokens, after a rollout of the first)
+    gives bit-identical rollouts to a fresh context: nothing of the first prefill, its cache layout
+    or its rollout plan leaks into the second."""
+    base = W.get("small_bf16")
+    w = W.scaled(base, f"reuse_{dtype}_{hd}", n_layers=2, d_model=256, n_heads=8, n_kv_heads=2,
+                 head_dim=hd, d_ffn=512, vocab=2048, feat_layers=(0, 1), dtype=dtype, n_seq=3,
+                 seq_len=300, block=5)
+    wts = W.random_weights(w.shape, 7 + hd, scale=0.05, norm_gain="random")
+    lens_a, lens_b = [300, 200, 100], [129, 300]
+    tok_a = W.random_tokens(2048, (3, 300), 1, dist="zipf")
+    tok_b = W.random_tokens(2048, (2, 300), 2, dist="zipf")
+    a_s_a, a_p_a = np.array([0, 1, 2, 0], np.int32), np.array([299, 150, 50, 10], np.int32)
+    a_s_b, a_p_b = np.array([1, 0, 1, 0], np.int32), np.array([299, 128, 0, 64], np.int32)
+    inp = W.Inputs(w, wts, tok_a, a_s_a, a_p_a, None, None)
+
+    def pf(e, tok, lens):
+        flat = np.concatenate([tok[q, :n] for q, n in enumerate(lens)]).astype(np.int32)
+        e.prefill(torch.from_numpy(flat).to(e.device), lens)
+
+    eng = make_engine(inp, max_anchors=8, max_block=w.block)
+    pf(eng, tok_a, lens_a)
+    runner(eng, a_s_a, a_p_a, w.block)(None)
+    pf(eng, tok_b, lens_b)
+    t1, l1, f1 = runner(eng, a_s_b, a_p_b, w.block)(None)
+    eng.close()
+    fresh = make_engine(inp, max_anchors=8, max_block=w.block)
+    pf(fresh, tok_b, lens_b)
+    t2, l2, f2 = runner(fresh, a_s_b, a_p_b, w.block)(None)
+    fresh.close()
+    np.testing.assert_array_equal(t1, t2)
+    np.testing.assert_array_equal(l1, l2)
+    np.testing.assert_array_equal(f1, f2)
+
+
 def test_rollout_before_prefill_is_a_state_error():
     inp = W.make_inputs("tiny_fp32")
     eng = make_engine(inp)
