@@ -18,13 +18,13 @@ from .reference import (  # noqa: F401
     bf16_round,
     rmsnorm,
     rope,
-    rope_angles,
     silu,
     causal_gqa_attention,
     log_softmax,
     greedy_argmax,
     embed_rows,
     decoder_forward,
+    decoder_layer_at,
     head_logits,
     prefill_outputs,
     rollout_naive,

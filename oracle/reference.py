@@ -129,14 +129,6 @@ def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
-def rope_angles(positions: np.ndarray, head_dim: int, base: float, dt=np.float64):
-    """cos and sin of pos * base^(-2i/head_dim) for i < head_dim/2, computed in float64."""
-    half = head_dim // 2
-    inv = np.power(float(base), -2.0 * np.arange(half, dtype=np.float64) / head_dim)
-    ang = np.asarray(positions, dtype=np.float64)[:, None] * inv[None, :]
-    return np.cos(ang).astype(dt), np.sin(ang).astype(dt)
-
-
 def rope_axis_of(half: int, sections) -> np.ndarray:
     """Position axis (0 = t, 1 = h, 2 = w) that drives frequency i < half under M-RoPE.
 
@@ -171,21 +163,24 @@ def rope(x: np.ndarray, positions: np.ndarray, base: float, sections=None) -> np
 
 
 def causal_gqa_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
-                         round_probs=None) -> np.ndarray:
-    """Causal softmax attention. q[T,H,hd], k/v[T,G,hd] -> out[T,H,hd].
+                         round_probs=None, q_pos=None) -> np.ndarray:
+    """Causal softmax attention. q[Tq,H,hd], k/v[T,G,hd] -> out[Tq,H,hd].
 
     Query head j reads key/value head j // (H/G); scores are scaled by
-    1/sqrt(hd); position t sees keys 0..t.  round_probs (optional): a rounding
-    applied to the unnormalised probabilities exp(s - max) where they multiply
-    the values, the normaliser staying in working precision (how a bf16
-    matrix-core attention evaluates the value product).
+    1/sqrt(hd); the query at position t sees keys 0..t.  q_pos[Tq] gives the
+    position of each query row among the key rows (default: query row t is at
+    position t, so Tq = T).  round_probs (optional): a rounding applied to the
+    unnormalised probabilities exp(s - max) where they multiply the values, the
+    normaliser staying in working precision (how a bf16 matrix-core attention
+    evaluates the value product).
     """
-    T, H, hd = q.shape
-    G = k.shape[1]
+    Tq, H, hd = q.shape
+    T, G = k.shape[0], k.shape[1]
     rep = H // G
+    qp = np.arange(Tq) if q_pos is None else np.asarray(q_pos, dtype=np.int64)
     out = np.empty_like(q)
     scale = 1.0 / np.sqrt(hd)
-    mask = np.triu(np.ones((T, T), dtype=bool), 1)
+    mask = np.arange(T)[None, :] > qp[:, None]
     for j in range(H):
         g = j // rep
         s = (q[:, j, :] @ k[:, g, :].T) * scale
@@ -258,6 +253,38 @@ def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
             outs.append(h.copy())
     hf = rnd(rmsnorm(h, P.get("final_norm"), eps))
     return outs, hf
+
+
+def decoder_layer_at(P: Params, shape, layer: int, x: np.ndarray, positions: np.ndarray,
+                     rows, emulate_bf16: bool = False, bf16_probs: bool = False) -> np.ndarray:
+    """Output of decoder layer ``layer`` at the sequence positions ``rows`` only.
+
+    x[T, d] is the layer's input at positions 0..T-1 (T > max(rows)) and
+    positions[T] or [T, 3] their RoPE positions.  Causality makes a row's
+    output depend on the keys and values of rows 0..row only, so keys and
+    values are formed for every row and everything else only for ``rows``:
+    the same arithmetic as one layer of :func:`decoder_forward`, restricted to
+    the rows asked for.  Returns [len(rows), d].
+    """
+    rnd = bf16_round if emulate_bf16 else _ident
+    rp = bf16_round if (emulate_bf16 and bf16_probs) else None
+    dt = P.dt
+    H, G, hd, eps = shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.rms_eps
+    rows = np.asarray(rows, dtype=np.int64)
+    T = int(rows.max()) + 1
+    h_all = x[:T].astype(dt)
+    pos = np.asarray(positions)[:T]
+    n1 = rnd(rmsnorm(h_all, P.get("attn_norm", layer), eps))
+    k = rnd(rope((n1 @ P.get("wk", layer).T).reshape(T, G, hd), pos, shape.rope_base,
+                 _sections(shape)))
+    v = rnd((n1 @ P.get("wv", layer).T).reshape(T, G, hd))
+    q = rnd(rope((n1[rows] @ P.get("wq", layer).T).reshape(len(rows), H, hd), pos[rows],
+                 shape.rope_base, _sections(shape)))
+    o = rnd(causal_gqa_attention(q, k, v, rp, q_pos=rows).reshape(len(rows), H * hd))
+    h = h_all[rows] + o @ P.get("wo", layer).T
+    n2 = rnd(rmsnorm(h, P.get("ffn_norm", layer), eps))
+    act = rnd(silu(n2 @ P.get("w_gate", layer).T) * (n2 @ P.get("w_up", layer).T))
+    return h + act @ P.get("w_down", layer).T
 
 
 def _sections(shape):

@@ -157,7 +157,8 @@ def test_greedy_corpus_hard_gate_is_one_and_kd_equals_rollout():
 
 
 def test_corpus_slot0_equals_rollout_slot0():
-    """Sec. 3.2: slot 1 receives identical supervision under KD, erase and ALR."""
+    """Sec. 3.2: the first draft slot's label is the same under corpus KD and ALR (both read
+    the target at the anchor itself, before any rollout token)."""
     shape = _tiny_shape(vocab=19)
     P = O.Params(W.random_weights(shape, 5, norm_gain="random", scale=0.4))
     toks = W.random_tokens(shape.vocab, (1, 20), 3)

@@ -193,6 +193,50 @@ def test_attention_matches_torch_sdpa():
                                rtol=1e-10, atol=1e-12)
 
 
+def test_attention_query_positions_select_rows():
+    """q_pos places a subset of query rows among the keys: each row equals the full causal
+    attention's row at that position (the scalar brute force decides both)."""
+    rng = np.random.default_rng(8)
+    q = rng.standard_normal((9, 4, 3))
+    k = rng.standard_normal((9, 2, 3))
+    v = rng.standard_normal((9, 2, 3))
+    rows = np.array([0, 4, 8])
+    ref = _scalar_attention(q, k, v)[rows]
+    np.testing.assert_allclose(O.causal_gqa_attention(q[rows], k, v, q_pos=rows), ref, rtol=1e-12)
+    # a query at position 4 ignores keys 5..8 entirely
+    k2 = k.copy(); k2[5:] = 1e3 * rng.standard_normal(k2[5:].shape)
+    np.testing.assert_allclose(O.causal_gqa_attention(q[[4]], k2, v, q_pos=[4]), ref[[1]],
+                               rtol=1e-12)
+
+
+@pytest.mark.parametrize("sections", [None, (1, 0, 1)])
+@pytest.mark.parametrize("emulate", [False, True])
+def test_layer_at_rows_equals_full_forward(sections, emulate):
+    """One decoder layer evaluated at chosen rows equals that layer of the full forward at
+    those rows (any slip in the restriction -- a query from the wrong row, keys past the row,
+    a residual from another row -- fails it).  Layer 1's input is layer 0's output."""
+    shape = tiny_shape(n_layers=2, head_dim=4, mrope_sections=sections or (0, 0, 0))
+    w = f64_weights(shape, 21)
+    P = O.Params(w)
+    T = 13
+    toks = W.random_tokens(shape.vocab, (1, T), 5)[0]
+    x0 = O.embed_rows(P, toks)
+    pos = np.arange(T) if sections is None else np.stack(
+        [np.arange(T), np.arange(T) // 3, np.arange(T) % 3 + 2], axis=1)
+    for probs in ([False, True] if emulate else [False]):
+        outs, _ = O.decoder_forward(P, shape, x0, pos, emulate_bf16=emulate, bf16_probs=probs)
+        for layer, x in ((0, x0), (1, outs[0])):
+            for rows in ([T - 1], [0, 5, 6, 12], list(range(T))):
+                got = O.decoder_layer_at(P, shape, layer, x, pos, rows, emulate_bf16=emulate,
+                                         bf16_probs=probs)
+                np.testing.assert_allclose(got, outs[layer][rows], rtol=1e-12, atol=1e-12)
+    # rows past the last asked-for one do not matter
+    x_mod = x0.copy()
+    x_mod[7:] += 5.0
+    np.testing.assert_allclose(O.decoder_layer_at(P, shape, 0, x_mod, pos, [2, 6]),
+                               O.decoder_layer_at(P, shape, 0, x0, pos, [2, 6]), rtol=0, atol=0)
+
+
 # ---------------------------------------------------------------- decoder layer closed forms
 def _hand_model():
     """d=2, one head of dim 2, F=1, V=3: every layer output computable by hand at T=1."""
