@@ -43,8 +43,8 @@ def site_work(site: str, w, anchor_seq=None, anchor_pos=None) -> dict:
         m, n, k = gemm[site]
         return {"bound": "mfma", "flops": 2.0 * m * n * k, "unit": "TFLOP/s"}
     if site == "lm_finalize":
-        # one fp32 read (max/argmax/sum-exp pass) and one read+write (log-softmax) per entry
-        return {"bound": "hbm", "bytes": 12.0 * NA * V, "unit": "GB/s"}
+        # the log-softmax rewrite of the logits: one fp32 read and one fp32 write per entry
+        return {"bound": "hbm", "bytes": 8.0 * NA * V, "unit": "GB/s"}
     if site == "decode_attn":
         # unique bytes of one launch, averaged over the rollout steps s = 1 .. B-1: every
         # sequence's shared K and V up to its last anchor, each anchor's s private keys and
@@ -101,16 +101,32 @@ def measured_traffic(site: str):
     return float(m_t.group(1))
 
 
-def cpu_baseline(inp, budget_layers=(2, 8), n_anchors=2):
-    """Time the oracle (teacher-forced, fp64) on the anchors with the shortest prefixes,
-    with the model cut to two depths; extrapolate linearly in depth to the full model."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(inp, budget_layers=(2, 4)):
+    """Time the oracle (teacher-forced, fp64, bf16-emulating) on the anchor with the median
+    prefix of the workload, with the model cut to two depths, and extrapolate to the full
+    depth: every decoder layer does the same work, so the time is affine in the depth (a
+    fixed part for the embedding and the output head plus one equal share per layer)."""
     import numpy as np
 
     import oracle as O
     from paper_2609_38795_amd import workloads as W
 
     w = inp.workload
-    sel = np.argsort(inp.anchor_pos, kind="stable")[:n_anchors]  # shortest prefixes
+    order = np.argsort(inp.anchor_pos, kind="stable")
+    sel = order[[len(order) // 2]]  # the median prefix
     a_seq, a_pos = inp.anchor_seq[sel], inp.anchor_pos[sel]
     feed = np.zeros((len(sel), w.block), np.int64)
     rows = mask = None
@@ -132,27 +148,28 @@ def cpu_baseline(inp, budget_layers=(2, 8), n_anchors=2):
     l1, l2 = min(l1, w.shape.n_layers), min(l2, w.shape.n_layers)
     if l1 == l2:
         t_full = times[l1]
-        return _cpu_result(w, t_full, len(sel), a_pos, times, l1, l2)
-    per_layer = (times[l2] - times[l1]) / (l2 - l1)
-    fixed = times[l1] - l1 * per_layer
-    t_full = fixed + w.shape.n_layers * per_layer
-    return _cpu_result(w, t_full, len(sel), a_pos, times, l1, l2)
-
-
-def _cpu_result(w, t_full, n, a_pos, times, l1, l2):
+    else:
+        per_layer = (times[l2] - times[l1]) / (l2 - l1)
+        fixed = times[l1] - l1 * per_layer
+        t_full = fixed + w.shape.n_layers * per_layer
     try:
         from threadpoolctl import threadpool_info
 
         cores = max(int(x.get("num_threads", 1)) for x in threadpool_info()) or 1
     except Exception:
         cores = os.cpu_count() or 1
+    n = len(sel)
+    extrap = (f"with the model cut to {l1} and {l2} decoder layers ({times[l1]:.1f} s, "
+              f"{times[l2]:.1f} s) and extrapolated to {w.shape.n_layers} layers "
+              f"({t_full:.1f} s; the time is affine in depth, and the median prefix makes the "
+              f"anchor representative of the workload's prefix lengths)"
+              if l1 != l2 else f"at full depth ({t_full:.1f} s)")
     return {"value": n * w.block / t_full, "unit": "rollout slots/s", "cores": cores,
-            "kind": "oracle",
-            "sample": (f"fp64 bf16-emulating teacher-forced oracle on the {n} anchors with the "
-                       f"shortest prefixes (positions {', '.join(str(int(p)) for p in a_pos)}; "
-                       f"{w.block} slots each) with the model cut to {l1} and {l2} decoder "
-                       f"layers ({times[l1]:.1f} s, {times[l2]:.1f} s), extrapolated linearly "
-                       f"to {w.shape.n_layers} layers ({t_full:.1f} s)")}
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "sample": (f"fp64 bf16-emulating teacher-forced oracle on the anchor with the median "
+                       f"prefix (position {int(a_pos[0])} of positions "
+                       f"{int(inp.anchor_pos.min())}..{int(inp.anchor_pos.max())}; {w.block} slots) "
+                       + extrap)}
 
 
 def main():

@@ -13,6 +13,11 @@ Parity rules (fp32 / bf16):
 * features: max-abs difference, divided by the RMS of the oracle's feature row
   for bf16, <= ``ft_tol``.
 
+Every report also carries the literal figures of the target contract, whatever
+the pass rule: absolute log-prob and feature max-abs, and, among the slots whose
+oracle margin exceeds the literal token threshold (1e-2 bf16, 1e-4 fp32), the
+share of all slots they make up and the share of them whose tokens match.
+
 The bf16 noise floor is the largest difference between the fp64 bf16 evaluation
 and another valid bf16 evaluation of the same model: one that rounds at the
 same points but accumulates in fp32, and one whose attention also rounds its
@@ -43,6 +48,15 @@ class Report:
     ft_tol: float
     tok_margin: float
     forced_rerun: bool
+    ft_abs: float = 0.0            # absolute feature max-abs (no RMS scaling)
+    lit_margin: float = 0.0        # literal token threshold: 1e-2 bf16, 1e-4 fp32
+    lit_checked: float = 0.0       # share of slots whose oracle margin exceeds it
+    lit_exact: float = 1.0         # share of those slots whose GPU token equals the oracle's
+
+    def literal(self) -> str:
+        return (f"literal: lp max-abs {self.lp_max_abs:.4g}, feature max-abs {self.ft_abs:.4g}, "
+                f"tokens bit-exact on {100 * self.lit_exact:.1f}% of the "
+                f"{100 * self.lit_checked:.1f}% of slots with margin > {self.lit_margin:g}")
 
     def ok(self) -> bool:
         return (self.lp_max_abs <= self.lp_tol and self.ft_max <= self.ft_tol
@@ -113,6 +127,7 @@ def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = Non
         chosen = o_lp[idx[0], idx[1], g_tok[idx]]
         confident_bad += int((chosen < top - tok_margin).sum())
     forced_rerun = False
+    o_tok_fin = o_tok
     if near.any():
         # continue on the oracle's path: feed the oracle's own tokens to both sides
         forced = o_tok.astype(np.int32).copy()
@@ -122,14 +137,21 @@ def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = Non
         conf = margin > tok_margin
         confident_bad += int(((g_tok != o_tok2) & conf).sum())
         forced_rerun = True
+        o_tok_fin = o_tok2
     lp_err = float(np.abs(g_lp - o_lp).max())
+    ft_abs = float(np.abs(g_ft - o_ft).max()) if o_ft.size else 0.0
     if o_ft.size:
         if bf16:
             rms = np.sqrt(np.mean(o_ft ** 2, axis=-1, keepdims=True))
             ft_err = float((np.abs(g_ft - o_ft) / rms).max())
         else:
-            ft_err = float(np.abs(g_ft - o_ft).max())
+            ft_err = ft_abs
     else:
         ft_err = 0.0
+    lit_margin = 1e-2 if bf16 else 1e-4
+    lit = margin > lit_margin
+    lit_checked = float(lit.mean())
+    lit_exact = float((g_tok[lit] == o_tok_fin[lit]).mean()) if lit.any() else 1.0
     return Report(int(np.prod(g_tok.shape)), lp_err, ft_err, confident_bad, int(near.sum()),
-                  floor_lp, floor_ft, lp_tol, ft_tol, tok_margin, forced_rerun)
+                  floor_lp, floor_ft, lp_tol, ft_tol, tok_margin, forced_rerun, ft_abs,
+                  lit_margin, lit_checked, lit_exact)
