@@ -3,16 +3,18 @@
  *
  * The library computes, for a fixed corpus and a set of anchor positions, the
  * target model's greedy continuation of every anchor's prefix, one draft block
- * long: Eq. 3 of Sec. 3.2 ("Labels from the target's rollout").  Following the
- * "Rollout implementation" paragraph of App. A ("Training Configuration"), one
- * forward pass over each corpus sequence (alr_prefill) fills a key/value cache
- * that all of that sequence's anchors share; each rollout step (alr_rollout)
- * then runs every anchor's newest token through the decoder as one batch, the
- * query of an anchor attending under one softmax to the cached corpus keys up
- * to its anchor and to its own rollout keys, kept in a separate per-anchor
- * buffer; labels are read from the final normalised hidden state through the
- * output head, greedy ties go to the lower token id, and the residual-stream
- * outputs of chosen layers are stored as features.
+ * long: Eq. 3 of Sec. 3.2 ("Labels from the target's rollout").  The structure
+ * is the one App. A ("Training Configuration", "Rollout implementation")
+ * describes.  alr_prefill runs the decoder once over each corpus sequence and
+ * keeps its keys and values as a cache that every anchor of that sequence
+ * reads.  alr_rollout then advances all anchors by one token per step, as one
+ * batch.  At each step an anchor's query is normalised in one softmax over two
+ * key sets: the cached corpus entries at positions up to the anchor, and the
+ * entries its own earlier rollout steps produced.  The second set lives in a
+ * buffer private to the anchor, so no corpus entry is duplicated per anchor.
+ * The next-token distribution comes from the final RMSNorm and the output
+ * head; the greedy pick is the lowest id among equal maxima; the residual
+ * stream after chosen layers is returned as features.
  *
  * Slot convention.  Slot s (0 <= s < block) of anchor a sits at position a+s.
  * Its input token is the corpus token x_a for s = 0 and the token fed after
@@ -32,6 +34,13 @@
  * SwiGLU output) are bf16; accumulation, residual stream, softmax statistics
  * and logits are fp32.  Log-probabilities and features are always returned in
  * fp32.
+ *
+ * Operand sizes (ALR_BF16).  The GEMM kernels address their operands with
+ * 32-bit byte offsets, so every activation operand, max(max_tokens,
+ * max_anchors) rows of max(d_model, d_ffn, n_heads*head_dim) bf16 values, and
+ * every weight matrix (vocab x d_model, 2*d_ffn x d_model, ...) must be smaller
+ * than 4 GiB; otherwise alr_create returns ALR_E_UNSUPPORTED and
+ * alr_workspace_bytes returns 0.
  *
  * Memory and ownership.  All device memory is owned by the caller: weights,
  * inputs, outputs and one workspace whose size alr_workspace_bytes() gives.
@@ -128,7 +137,8 @@ typedef struct {
 } alr_limits;
 
 /* Bytes of device workspace a context with this config and these limits needs.
- * Returns 0 if the config or limits are invalid.  Host only, no GPU needed. */
+ * Returns 0 if the config or limits are invalid or a GEMM operand would reach
+ * 4 GiB (see "Operand sizes").  Host only, no GPU needed. */
 size_t alr_workspace_bytes(const alr_config* cfg, const alr_limits* lim);
 
 /* Validate cfg (host only, no GPU needed).  On failure writes a message into

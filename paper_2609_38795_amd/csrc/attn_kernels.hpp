@@ -454,34 +454,6 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
   }
 }
 
-// Sum / max over each aligned group of LPH (8 or 16) lanes with DPP lane
-// permutations inside the 16-lane rows (no LDS round trip): the row (half)
-// mirror pairs lane i with its reflection, then the two quad swaps finish the
-// group.  Every lane of a group ends with the same bits (each step combines
-// a lane with its partner symmetrically).
-template <int CTRL>
-__device__ __forceinline__ float dpp_perm(float v) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-template <int LPH>
-__device__ __forceinline__ float group_sum(float v) {
-  static_assert(LPH == 8 || LPH == 16, "lanes per group");
-  if constexpr (LPH == 16) v += dpp_perm<0x140>(v);  // row_mirror
-  v += dpp_perm<0x141>(v);                           // row_half_mirror
-  v += dpp_perm<0xB1>(v);                            // quad_perm [1,0,3,2]
-  v += dpp_perm<0x4E>(v);                            // quad_perm [2,3,0,1]
-  return v;
-}
-template <int LPH>
-__device__ __forceinline__ float group_max(float v) {
-  static_assert(LPH == 8 || LPH == 16, "lanes per group");
-  if constexpr (LPH == 16) v = fmaxf(v, dpp_perm<0x140>(v));
-  v = fmaxf(v, dpp_perm<0x141>(v));
-  v = fmaxf(v, dpp_perm<0xB1>(v));
-  v = fmaxf(v, dpp_perm<0x4E>(v));
-  return v;
-}
-
 // Group of sorted anchors as the combine kernel sees it.
 struct DecodeGroup {
   int first, nchunk, part0;  // part index of (kv head 0, chunk 0); kv head g adds g*nchunk

@@ -74,4 +74,61 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Sum / max over each aligned group of LPH (8 or 16) lanes with DPP lane
+// permutations inside the 16-lane rows (no LDS round trip): the row (half)
+// mirror pairs lane i with its reflection, then the two quad swaps finish the
+// group.  Every lane of a group ends with the same bits (each step combines
+// a lane with its partner symmetrically).
+template <int CTRL>
+__device__ __forceinline__ float dpp_perm(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int LPH>
+__device__ __forceinline__ float group_sum(float v) {
+  static_assert(LPH == 8 || LPH == 16, "lanes per group");
+  if constexpr (LPH == 16) v += dpp_perm<0x140>(v);  // row_mirror
+  v += dpp_perm<0x141>(v);                           // row_half_mirror
+  v += dpp_perm<0xB1>(v);                            // quad_perm [1,0,3,2]
+  v += dpp_perm<0x4E>(v);                            // quad_perm [2,3,0,1]
+  return v;
+}
+template <int LPH>
+__device__ __forceinline__ float group_max(float v) {
+  static_assert(LPH == 8 || LPH == 16, "lanes per group");
+  if constexpr (LPH == 16) v = fmaxf(v, dpp_perm<0x140>(v));
+  v = fmaxf(v, dpp_perm<0x141>(v));
+  v = fmaxf(v, dpp_perm<0xB1>(v));
+  v = fmaxf(v, dpp_perm<0x4E>(v));
+  return v;
+}
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_perm_i(int v) {
+  return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ int group_min16_i(int v) {
+  v = min(v, dpp_perm_i<0x140>(v));
+  v = min(v, dpp_perm_i<0x141>(v));
+  v = min(v, dpp_perm_i<0xB1>(v));
+  v = min(v, dpp_perm_i<0x4E>(v));
+  return v;
+}
+
+// max / sum / min of v over lanes i and i ^ 16 (the two 16-lane rows of each
+// 32-lane half): v_permlane16_swap exchanges rows 0 <-> 1 and 2 <-> 3 in
+// registers; the pair it returns holds both rows' values in every lane.  Both
+// rows of a half must be active.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ int min_xor16_i(int v) {
+  const auto r = __builtin_amdgcn_permlane16_swap((unsigned)v, (unsigned)v, false, false);
+  return min((int)r[0], (int)r[1]);
+}
+
 }  // namespace alr

@@ -237,16 +237,50 @@ struct EpiSwiGLU {
   }
 };
 
-// Plain fp32 store of logits into caller rows: out + (perm ? perm[row] : row) * rs.
+// Per-row statistics of the output-head logits over one 64-column group: the
+// group's max m, s = sum of exp(z - m) over its 64 entries, and the lowest
+// column holding the max.  The finalisation merges a row's groups into its
+// log-sum-exp and argmax without another pass over the logits.
+struct LogitPart {
+  float m, s;
+  int i;
+};
+
+// LogitPart of one row over the 64-column group held by a 32-lane half-wave:
+// lane lr of the half holds column c = 64 g + lr (lo) and c + 32 (hi).  Every
+// lane of the half must call this with the same row; the result is the same
+// in all of them.
+__device__ __forceinline__ LogitPart half_wave_part(float lo, float hi, int c) {
+  float mx = group_max<16>(fmaxf(lo, hi));
+  mx = max_xor16(mx);
+  int arg = (lo == mx) ? c : ((hi == mx) ? c + 32 : 0x7FFFFFFF);
+  arg = min_xor16_i(group_min16_i(arg));
+  const float l2e = 1.44269504088896341f;
+  float e = fast_exp2((lo - mx) * l2e) + fast_exp2((hi - mx) * l2e);
+  e = sum_xor16(group_sum<16>(e));
+  return {mx, e, arg};
+}
+
+// fp32 logits into caller rows: out + (perm ? perm[row] : row) * rs; with part,
+// also the row's LogitPart of each 64-column group into part[row * part_ld + c / 64].
+// Every call site hands a 64-column group of one row to one 32-lane half-wave
+// (gemm_store_tile, gemm_f32_kernel), which the partials rely on; split-K is
+// not used for this epilogue when part is set.
 struct EpiLogits {
   float* out;
   long rs;
   const int* perm;
+  LogitPart* part;
+  int part_ld;
   __device__ __forceinline__ void operator()(int row, int c, float lo, float hi) const {
     const long r = perm ? perm[row] : row;
     float* p = out + r * rs + c;
     p[0] = lo;
     p[32] = hi;
+    if (part) {
+      const LogitPart q = half_wave_part(lo, hi, c);
+      if ((threadIdx.x & 31) == 0) part[(long)row * part_ld + (c >> 6)] = q;
+    }
   }
   __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
                                          const float* hi) const {
@@ -263,6 +297,18 @@ struct EpiLogits {
         p[0] = lo[t];
         p[32] = hi[t];
       }
+    if (part) {
+      // all 16 rows reduced over the half-wave; lane lr < 16 then stores row t = lr
+      const int lr = threadIdx.x & 31;
+      LogitPart mine = {0.f, 0.f, 0};
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const LogitPart q = half_wave_part(lo[t], hi[t], c);
+        if (lr == t) mine = q;
+      }
+      const int r = rb + 8 * (lr >> 2) + (lr & 3);
+      if (lr < 16 && r < M) part[(long)r * part_ld + (c >> 6)] = mine;
+    }
   }
 };
 

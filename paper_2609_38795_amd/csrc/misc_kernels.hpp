@@ -4,6 +4,7 @@
 #pragma once
 
 #include "device_common.hpp"
+#include "gemm_kernels.hpp"
 
 namespace alr {
 
@@ -140,12 +141,16 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(char* __restrict__ ds
 // Output head finalisation of the sorted row r of slot s.
 //   Logits (fp32, V entries) of row r are at z + (z_perm ? perm[r] : r) * z_rs,
 //   written by the output-head GEMM.  Outputs go to index o = perm[r] * block + s
-//   (the caller's anchor order).  Pass 1 computes the max, the argmax (ties ->
-//   lowest id) and sum(exp(z - max)); with TOPK it also keeps each thread's 8
-//   best (value, id) pairs, ranked by decreasing value and then increasing id,
-//   and merges them into the row's top 8 with eight block-wide argmax rounds.
-//   Pass 2 (when write_lp or TOPK) rewrites the row as z - LSE and, with TOPK,
-//   sums exp(z - max) over the tokens ranked after the 8th (the tail bucket).
+//   (the caller's anchor order).  The row's max, argmax (ties -> lowest id) and
+//   sum(exp(z - max)) come from the GEMM epilogue's per-group partials
+//   (part[r * part_ld + g], g < part_ld = V / 64) when part is set, else from a
+//   first pass over the logits.  Then one pass (when write_lp or TOPK) rewrites
+//   the row as z - LSE and, with TOPK, keeps each thread's 8 best (value, id)
+//   pairs, ranked by decreasing value and then increasing id, while summing
+//   exp(z - max) over every entry the thread drops from (or never admits to)
+//   that list; eight block-wide argmax rounds merge the lists into the row's
+//   top 8, and the entries left in the lists join the sum, which is then the
+//   mass of exactly the tokens ranked after the 8th (the tail bucket).
 //   next_tok[r] = forced[o] if that is >= 0, else the argmax.  target_logp[o]
 //   = log p(target[r]) (nan when target[r] < 0).  A row with valid[r] == 0 gets
 //   token -1, top ids -1, top log-probs -inf, tail 0, target log-prob nan and,
@@ -168,6 +173,8 @@ struct LmFinalize {
   const int* target;   // [r] or null
   float* target_logp;  // [o] (with target)
   const unsigned char* valid;  // [r] or null
+  const LogitPart* part;       // [r * part_ld + g] or null
+  int part_ld;
 };
 
 struct MaxArg {
@@ -217,44 +224,23 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
     return;
   }
   MaxArg acc = {-INFINITY, 0.f, 0x7FFFFFFF};
-  float tv[ALR_K_TOP];
-  int ti[ALR_K_TOP];
+  if (a.part != nullptr) {
+    const LogitPart* pr = a.part + (long)r * a.part_ld;
+    for (int g = threadIdx.x; g < a.part_ld; g += blockDim.x) {
+      const LogitPart q = pr[g];
+      acc = merge_maxarg(acc, MaxArg{q.m, q.s, q.i});
+    }
+  } else {
+    for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
+      const f32x4 v = *(const f32x4*)(z + c);
 #pragma unroll
-  for (int j = 0; j < ALR_K_TOP; ++j) {
-    tv[j] = -INFINITY;
-    ti[j] = 0x7FFFFFFF;
-  }
-  for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
-    const f32x4 v = *(const f32x4*)(z + c);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (v[e] > acc.m) {
-        acc.s = (acc.m == -INFINITY) ? 1.f : acc.s * expf(acc.m - v[e]) + 1.f;
-        acc.m = v[e];
-        acc.i = c + e;
-      } else {
-        acc.s += expf(v[e] - acc.m);
-      }
-      if constexpr (TOPK) {
-        // this thread meets ids in increasing order, so an equal value ranks
-        // after the entries already held: insert only strictly larger values
-        if (v[e] > tv[ALR_K_TOP - 1]) {
-          float pv = v[e];
-          int pi = c + e;
-          bool sh = false;
-#pragma unroll
-          for (int j = 0; j < ALR_K_TOP; ++j) {
-            const bool take = sh || (v[e] > tv[j]);
-            if (take) {
-              const float ov = tv[j];
-              const int oi = ti[j];
-              tv[j] = pv;
-              ti[j] = pi;
-              pv = ov;
-              pi = oi;
-            }
-            sh = take;
-          }
+      for (int e = 0; e < 4; ++e) {
+        if (v[e] > acc.m) {
+          acc.s = (acc.m == -INFINITY) ? 1.f : acc.s * expf(acc.m - v[e]) + 1.f;
+          acc.m = v[e];
+          acc.i = c + e;
+        } else {
+          acc.s += expf(v[e] - acc.m);
         }
       }
     }
@@ -288,6 +274,54 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
       const int x = a.target[r];
       tgt_sh = (x >= 0) ? z[x] : __builtin_nanf("");
     }
+  }
+  __syncthreads();
+  const float lse = lse_sh, m = m_sh;
+  if (!a.write_lp && !TOPK) {
+    if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
+    return;
+  }
+  float tv[ALR_K_TOP];
+  int ti[ALR_K_TOP];
+#pragma unroll
+  for (int j = 0; j < ALR_K_TOP; ++j) {
+    tv[j] = -INFINITY;
+    ti[j] = 0x7FFFFFFF;
+  }
+  float tsum = 0.f;  // exp(z - m) of the entries this thread dropped or never admitted
+  for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
+    f32x4 v = *(const f32x4*)(z + c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (TOPK) {
+        // this thread meets ids in increasing order, so an equal value ranks
+        // after the entries already held: admit only strictly larger values
+        if (v[e] > tv[ALR_K_TOP - 1]) {
+          const float out_v = tv[ALR_K_TOP - 1];
+          if (out_v != -INFINITY) tsum += expf(out_v - m);
+          float pv = v[e];
+          int pi = c + e;
+          bool sh = false;
+#pragma unroll
+          for (int j = 0; j < ALR_K_TOP; ++j) {
+            const bool take = sh || (v[e] > tv[j]);
+            if (take) {
+              const float ov = tv[j];
+              const int oi = ti[j];
+              tv[j] = pv;
+              ti[j] = pi;
+              pv = ov;
+              pi = oi;
+            }
+            sh = take;
+          }
+        } else {
+          tsum += expf(v[e] - m);
+        }
+      }
+      v[e] -= lse;
+    }
+    if (a.write_lp) *(f32x4*)(z + c) = v;
   }
   if constexpr (TOPK) {
     // eight rounds: the best head of all threads' lists is the next entry
@@ -330,29 +364,10 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
         ti[ALR_K_TOP - 1] = 0x7FFFFFFF;
       }
     }
-  } else {
-    __syncthreads();
-  }
-  const float lse = lse_sh, m = m_sh;
-  if (!a.write_lp && !TOPK) {
-    if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
-    return;
-  }
-  const float zk = TOPK ? top_v[ALR_K_TOP - 1] : 0.f;
-  const int ik = TOPK ? top_i[ALR_K_TOP - 1] : 0;
-  float tsum = 0.f;
-  for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
-    f32x4 v = *(const f32x4*)(z + c);
+    // what is left in the lists ranks after the 8th entry
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if constexpr (TOPK) {
-        if (v[e] < zk || (v[e] == zk && c + e > ik)) tsum += expf(v[e] - m);
-      }
-      v[e] -= lse;
-    }
-    if (a.write_lp) *(f32x4*)(z + c) = v;
-  }
-  if constexpr (TOPK) {
+    for (int j = 0; j < ALR_K_TOP; ++j)
+      if (tv[j] != -INFINITY) tsum += expf(tv[j] - m);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) tsum += __shfl_xor(tsum, off);
     if (lane == 0) tail_red[wave] = tsum;

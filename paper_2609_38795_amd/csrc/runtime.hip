@@ -53,7 +53,7 @@ struct Layout {
   size_t feat_store, hf_store;
   size_t resid, xnorm, qbuf, attn, act;
   size_t i_tokpos, i_rowstart, i_perm, i_apos, i_rpos, i_atok, i_aseq, i_alen, i_cur;
-  size_t i_valid, i_target, i_ira, i_ctok, logits;
+  size_t i_valid, i_target, i_ira, i_ctok, logits, lm_part;
   size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
   size_t splitk, splitk_bytes;
@@ -121,6 +121,30 @@ alr_status check_limits(const alr_limits* l, char* msg, size_t len) {
   if (!l) return fmt_msg(msg, len, "limits is NULL"), ALR_E_INVALID_ARG;
   if (l->max_tokens <= 0 || l->max_seqs <= 0 || l->max_anchors <= 0 || l->max_block <= 0)
     return fmt_msg(msg, len, "limits must be positive"), ALR_E_INVALID_ARG;
+  return ALR_OK;
+}
+
+// The bf16 GEMM kernels address a thread's operand chunks by 32-bit byte
+// offsets from the operand base, so every GEMM operand (activation rows of
+// max(max_tokens, max_anchors) x K, weight matrices N x K) must stay below
+// 4 GiB.  cfg and lim are already valid.
+alr_status check_operand_sizes(const alr_config& c, const alr_limits& lim, char* msg, size_t len) {
+  if (c.dtype != ALR_BF16) return ALR_OK;
+  const double lim32 = 4294967296.0;
+  const double d = c.d_model, F = c.d_ffn, V = c.vocab;
+  const double qd = (double)c.n_heads * c.head_dim, kvd = (double)c.n_kv_heads * c.head_dim;
+  const double R = std::max(lim.max_tokens, lim.max_anchors);
+  const double act = R * std::max(std::max(d, F), qd) * 2.0;
+  const double wmax = std::max(std::max(V * d, 2.0 * F * d), std::max((qd + 2 * kvd) * d, d * F)) * 2.0;
+  if (act >= lim32)
+    return fmt_msg(msg, len,
+                   "GEMM activation operand of %.0f rows x %.0f bf16 is >= 4 GiB (lower max_tokens "
+                   "/ max_anchors)",
+                   R, std::max(std::max(d, F), qd)),
+           ALR_E_UNSUPPORTED;
+  if (wmax >= lim32)
+    return fmt_msg(msg, len, "a weight matrix of the config is >= 4 GiB in bf16"),
+           ALR_E_UNSUPPORTED;
   return ALR_OK;
 }
 
@@ -196,6 +220,8 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_ira = take(NA * 2 * 4);
   L.i_ctok = take(T * 4);
   L.logits = take(NA * V * 4);
+  // output-head partials: one LogitPart per (anchor row, 64-column group)
+  L.lm_part = take(NA * (V / 64) * sizeof(LogitPart));
   L.max_pwork = ((T + 31) / 32 + lim.max_seqs) * H + (size_t)lim.max_seqs * G;
   const size_t ag = (size_t)anchor_group(c);
   L.max_groups = (NA + ag - 1) / ag + std::min<size_t>(lim.max_seqs, NA);
@@ -361,7 +387,11 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     // GEMMs take the 128x128 kernel with the epilogue fused.  With uneven
     // rounds (N = 6144: 384 tiles on 256 CUs) split-K stays ahead.
     const bool fill128 = K <= 4096 && tiles(128, 128) % ctx->n_cu == 0;
-    if ((cfg == 18 || (cfg == 0 && !fill128)) && ctx->splitk_buf != nullptr) {
+    // the output head's per-group partials are formed in the epilogue of each
+    // tile; a split-K reduce hands it columns in another arrangement
+    bool epi_whole_k = false;
+    if constexpr (std::is_same<Epi, EpiLogits>::value) epi_whole_k = epi.part != nullptr;
+    if ((cfg == 18 || (cfg == 0 && !fill128)) && ctx->splitk_buf != nullptr && !epi_whole_k) {
       const int t256 = tiles(256, 256);
       int S = 1;
       for (int cand : {2, 4})
@@ -641,6 +671,10 @@ alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, con
   const int* perm = ctx->at<int>(L.i_perm);
   EpiLogits el;
   LmFinalize f;
+  el.part = ctx->at<LogitPart>(L.lm_part);
+  el.part_ld = V / 64;
+  f.part = el.part;
+  f.part_ld = el.part_ld;
   if (out.logprobs) {
     el.out = out.logprobs + (long)s * V;
     el.rs = (long)block * V;
@@ -773,7 +807,8 @@ alr_status alr_check_config(const alr_config* cfg, char* msg, size_t msg_len) {
 }
 
 size_t alr_workspace_bytes(const alr_config* cfg, const alr_limits* lim) {
-  if (check_config_impl(cfg, nullptr, 0) != ALR_OK || check_limits(lim, nullptr, 0) != ALR_OK)
+  if (check_config_impl(cfg, nullptr, 0) != ALR_OK || check_limits(lim, nullptr, 0) != ALR_OK ||
+      check_operand_sizes(*cfg, *lim, nullptr, 0) != ALR_OK)
     return 0;
   Layout L;
   return compute_layout(*cfg, *lim, L);
@@ -801,6 +836,8 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
   alr_status st = check_config_impl(cfg, msg, sizeof(msg));
   if (st != ALR_OK) return fail(nullptr, st, "%s", msg);
   st = check_limits(lim, msg, sizeof(msg));
+  if (st != ALR_OK) return fail(nullptr, st, "%s", msg);
+  st = check_operand_sizes(*cfg, *lim, msg, sizeof(msg));
   if (st != ALR_OK) return fail(nullptr, st, "%s", msg);
   const alr_config& c = *cfg;
   if (!w || !w->tok_embed || !w->final_norm || !w->lm_head)
@@ -1435,6 +1472,8 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   el.out = C;
   el.rs = N;
   el.perm = nullptr;
+  el.part = nullptr;
+  el.part_ld = 0;
   alr_ctx dummy;
   if (dtype == ALR_BF16) {
     const bf16* Wk = (const bf16*)W;

@@ -136,3 +136,28 @@ def test_rollout_and_prefill_reject_null_context(lib):
     assert lib.alr_rollout(None, 1, binding._i32p(z), binding._i32p(z), 1, None, None, None,
                            None, None) == 1
     assert lib.alr_prefill(None, 1, binding._i32p(z), None, None, None, None, None) == 1
+
+
+def test_operands_of_4gib_are_rejected(lib):
+    """The bf16 GEMM kernels address operand chunks by 32-bit byte offsets: a context whose
+    activation operand (max(max_tokens, max_anchors) rows of max(d, F, H hd) bf16) or any weight
+    matrix reaches 4 GiB is refused before anything is allocated or launched."""
+    w, cfg = _cfg("llama8b_like")
+    F = w.shape.d_ffn
+    r_ok = (2 ** 32 - 1) // (2 * F)  # largest row count whose F-wide bf16 operand is < 4 GiB
+    ok = binding.make_limits(r_ok, 8, 1024, 16)
+    assert lib.alr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(ok)) > 0
+    for lim in (binding.make_limits(r_ok + 1, 8, 1024, 16),
+                binding.make_limits(4096, 8, r_ok + 1, 16)):
+        assert lib.alr_workspace_bytes(ctypes.byref(cfg), ctypes.byref(lim)) == 0
+        ctx = ctypes.c_void_p()
+        st = lib.alr_create(ctypes.byref(cfg), ctypes.byref(binding.AlrWeights()), ctypes.byref(lim),
+                            None, 0, None, ctypes.byref(ctx))
+        assert st == 5 and not ctx.value
+        assert b"4 GiB" in lib.alr_last_error(None)
+    # a weight matrix of 4 GiB: vocab x d_model bf16
+    big = binding.make_config(W.scaled(w, "x", vocab=2 ** 31 // w.shape.d_model).shape, w.max_pos)
+    assert lib.alr_workspace_bytes(ctypes.byref(big), ctypes.byref(ok)) == 0
+    # fp32 contexts use the FMA kernel with 64-bit offsets: no such limit
+    wf, cf = _cfg("tiny_fp32")
+    assert lib.alr_workspace_bytes(ctypes.byref(cf), ctypes.byref(binding.make_limits(200000, 1, 8, 4))) > 0
