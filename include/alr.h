@@ -230,6 +230,31 @@ alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* ancho
                             float* tail_out, float* logprobs_out, float* feats_out,
                             alr_stream stream);
 
+/* Bytes of the fixed device array behind alr_rollout_topk_noalloc (64 MiB). */
+#define ALR_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* alr_rollout_topk for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same arguments, checks and results as alr_rollout_topk with
+ * logprobs_out = NULL, but the per-step scratch -- each step's fp32 logit rows
+ * [n_anchor, vocab] and their per-64-column log-sum-exp partials [n_anchor,
+ * vocab/64] of 12 bytes -- lives in a fixed array of ALR_NOALLOC_SCRATCH_BYTES
+ * that the library holds on every device it runs on until the process ends
+ * (its address is looked up once per device by alr_create), not in the
+ * context's workspace.  The call allocates nothing and frees nothing.
+ *   Limit: 256-byte-aligned n_anchor * vocab * 4 plus n_anchor * (vocab/64) * 12
+ *   must fit in the array (e.g. 128 anchors at vocab 128256, 500 at 32000);
+ *   larger requests return ALR_E_WORKSPACE before anything is enqueued.
+ * Every entry of the scratch a call reads is first written by that call, so
+ * nothing needs clearing between calls.  All calls on one device share the one
+ * array: calls whose execution overlaps on a device (other streams, other
+ * contexts, other threads) race on it and must be serialised by the caller. */
+alr_status alr_rollout_topk_noalloc(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                                    const int32_t* anchor_pos, int32_t block,
+                                    const int32_t* forced, int32_t* tokens_out,
+                                    int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                                    float* feats_out, alr_stream stream);
+
 /* Fixed-corpus distillation labels and erase gates (Sec. 3.1: the KD labels
  * pi_{a,k} = p_T(. | x_{<a+k}), and Eq. 2, the survival gate with its hard
  * variant), read from the last prefill's final normalised rows through the

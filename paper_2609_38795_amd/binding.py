@@ -24,6 +24,7 @@ STATUS = {0: "ALR_OK", 1: "ALR_E_INVALID_ARG", 2: "ALR_E_OUT_OF_RANGE", 3: "ALR_
 # Every function the C headers declare (include/alr.h, include/alr_debug.h).
 EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_create",
            "alr_prefill", "alr_prefill_positions", "alr_rollout", "alr_rollout_topk",
+           "alr_rollout_topk_noalloc",
            "alr_corpus_labels", "alr_ira_assemble", "alr_slot_weights", "alr_last_error", "alr_status_string", "alr_destroy",
            "alr_debug_gemm", "alr_debug_decode_plan", "alr_profile_start", "alr_profile_stop")
 ALR_TOPK = 8
@@ -96,6 +97,8 @@ def load_library() -> ctypes.CDLL:
     lib.alr_rollout.restype = ctypes.c_int
     lib.alr_rollout_topk.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.alr_rollout_topk.restype = ctypes.c_int
+    lib.alr_rollout_topk_noalloc.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.alr_rollout_topk_noalloc.restype = ctypes.c_int
     lib.alr_corpus_labels.argtypes = [vp, i32, i32p, i32p, i32, vp, vp, vp, vp, vp, vp, vp, vp,
                                       vp]
     lib.alr_corpus_labels.restype = ctypes.c_int
@@ -330,6 +333,20 @@ class Engine:
         if st != 0:
             self._err(st)
         return tok, ti, tl, tt, lp, ft
+
+    def rollout_topk_noalloc(self, anchor_seq, anchor_pos, block: int, out, forced=None):
+        """alr_rollout_topk_noalloc into caller tensors out = (tokens, top_ids, top_logp, tail,
+        feats or None); the library's fixed scratch holds the per-step logits."""
+        a_s = np.ascontiguousarray(anchor_seq, dtype=np.int32)
+        a_p = np.ascontiguousarray(anchor_pos, dtype=np.int32)
+        tok, ti, tl, tt, ft = out
+        st = self.lib.alr_rollout_topk_noalloc(
+            self.ctx, len(a_s), _i32p(a_s), _i32p(a_p), block,
+            None if forced is None else forced.data_ptr(), tok.data_ptr(), ti.data_ptr(),
+            tl.data_ptr(), tt.data_ptr(), None if ft is None else ft.data_ptr(), self._sp())
+        if st != 0:
+            self._err(st)
+        return tok, ti, tl, tt, ft
 
     def corpus_labels(self, anchor_seq, anchor_pos, block: int, want_topk: bool = True,
                       want_logprobs: bool = False):

@@ -19,6 +19,7 @@
 #include <cstdio>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <numeric>
 #include <queue>
 #include <string>
@@ -303,6 +304,8 @@ struct alr_ctx {
   bool prefilled = false;
   int n_cu = 256;  // compute units of the device (sizes the decode work split)
   float* splitk_buf = nullptr;  // split-K partial sums (workspace)
+  char* noalloc_scratch = nullptr;  // device address of `scratch` on the context's device
+  std::string noalloc_err;          // why it could not be looked up, if it could not
   size_t splitk_bytes = 0;
   int n_seq = 0;
   std::vector<int> seq_len, seq_off;
@@ -323,7 +326,34 @@ struct alr_ctx {
   char* layer(int l) const { return ws + L.layer0 + (size_t)l * L.layer_stride; }
 };
 
+// Scratch of alr_rollout_topk_noalloc (each step's logit rows and their
+// per-group partials), for callers that cannot allocate device memory.  Every
+// device the library runs on holds its own copy until the process ends.  In
+// host code this name is only a handle for hipGetSymbolAddress: kernels get the
+// device address that call returns (noalloc_scratch_address).
+static __device__ __align__(256) char scratch[ALR_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+std::mutex g_scratch_mu;
+std::vector<char*> g_scratch_addr;  // per device ordinal, looked up once
+
+// Device address of `scratch` on the current device.
+hipError_t noalloc_scratch_address(char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if ((int)g_scratch_addr.size() <= dev) g_scratch_addr.resize(dev + 1, nullptr);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
 
 alr_status fail(alr_ctx* ctx, alr_status st, const char* f, ...) {
   char buf[512];
@@ -651,11 +681,13 @@ alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* 
 
 // Output destinations of the labels of one rollout or corpus-label call.
 struct LabelDst {
-  float* logprobs;  // [n, block, V] or null (then the logits go to the workspace)
+  float* logprobs;  // [n, block, V] or null (then the logits go to the logit rows below)
   int* tokens;      // argmax per slot [n, block]
   int* top_ids;     // [n, block, 8] or null (no top-8 labels)
   float* top_logp;
   float* tail;
+  float* logit_rows = nullptr;      // [n, V] scratch for the logits; null: the workspace's
+  LogitPart* part_rows = nullptr;   // [n, V/64] scratch for the partials; null: the workspace's
 };
 
 // Output head of slot s for the n sorted rows in xnorm: logits GEMM (into the
@@ -671,7 +703,7 @@ alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, con
   const int* perm = ctx->at<int>(L.i_perm);
   EpiLogits el;
   LmFinalize f;
-  el.part = ctx->at<LogitPart>(L.lm_part);
+  el.part = out.part_rows ? out.part_rows : ctx->at<LogitPart>(L.lm_part);
   el.part_ld = V / 64;
   f.part = el.part;
   f.part_ld = el.part_ld;
@@ -684,10 +716,11 @@ alr_status lm_head(alr_ctx* ctx, int n, int s, int block, const int* forced, con
     f.z_perm = 1;
     f.write_lp = 1;
   } else {
-    el.out = ctx->at<float>(L.logits);
+    float* rows = out.logit_rows ? out.logit_rows : ctx->at<float>(L.logits);
+    el.out = rows;
     el.rs = V;
     el.perm = nullptr;
-    f.z = ctx->at<float>(L.logits);
+    f.z = rows;
     f.z_rs = V;
     f.z_perm = 0;
     f.write_lp = 0;
@@ -883,6 +916,15 @@ alr_status alr_create(const alr_config* cfg, const alr_weights* w, const alr_lim
     CREATE_HIP(hipGetDevice(&dev));
     CREATE_HIP(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
     ctx->n_cu = std::max(1, ncu);
+  }
+  {
+    // with the context's device current: the no-alloc entry point's scratch
+    const hipError_t e = noalloc_scratch_address(&ctx->noalloc_scratch);
+    if (e != hipSuccess) {
+      ctx->noalloc_scratch = nullptr;
+      ctx->noalloc_err = hipGetErrorString(e);
+      (void)hipGetLastError();
+    }
   }
   ctx->splitk_buf = ctx->at<float>(L.splitk);
   ctx->splitk_bytes = L.splitk_bytes;
@@ -1309,6 +1351,40 @@ alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* ancho
              : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
 }
 
+alr_status alr_rollout_topk_noalloc(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
+                                    const int32_t* anchor_pos, int32_t block,
+                                    const int32_t* forced, int32_t* tokens_out,
+                                    int32_t* top_ids_out, float* top_logp_out, float* tail_out,
+                                    float* feats_out, alr_stream stream) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (!tokens_out || !top_ids_out || !top_logp_out || !tail_out)
+    return fail(ctx, ALR_E_INVALID_ARG,
+                "tokens_out, top_ids_out, top_logp_out and tail_out must not be NULL");
+  const size_t V = (size_t)ctx->cfg.vocab;
+  const size_t per_row = V * 4 + (V / 64) * sizeof(LogitPart);
+  if (n_anchor > 0 && align256((size_t)n_anchor * V * 4) +
+                          (size_t)n_anchor * (V / 64) * sizeof(LogitPart) >
+                      (size_t)ALR_NOALLOC_SCRATCH_BYTES)
+    return fail(ctx, ALR_E_WORKSPACE,
+                "n_anchor %d needs %zu bytes of scratch at vocab %zu, more than the %zu-byte "
+                "no-alloc scratch (at most %zu anchors)",
+                n_anchor, (size_t)n_anchor * per_row, V, (size_t)ALR_NOALLOC_SCRATCH_BYTES,
+                ((size_t)ALR_NOALLOC_SCRATCH_BYTES - 256) / per_row);
+  if (!ctx->noalloc_scratch)
+    return fail(ctx, ALR_E_HIP, "scratch address lookup failed at alr_create: %s",
+                ctx->noalloc_err.c_str());
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  alr_status st = prepare_anchors(ctx, n_anchor, anchor_seq, anchor_pos, block, true, s);
+  if (st != ALR_OK) return st;
+  LabelDst out{nullptr, tokens_out, top_ids_out, top_logp_out, tail_out};
+  out.logit_rows = reinterpret_cast<float*>(ctx->noalloc_scratch);
+  out.part_rows = reinterpret_cast<LogitPart*>(ctx->noalloc_scratch +
+                                               align256((size_t)n_anchor * V * 4));
+  return (ctx->cfg.dtype == ALR_BF16)
+             ? rollout_impl<bf16>(ctx, n_anchor, block, forced, out, feats_out, s)
+             : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
+}
+
 alr_status alr_corpus_labels(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
                              const int32_t* anchor_pos, int32_t block, int32_t* argmax_out,
                              int32_t* top_ids_out, float* top_logp_out, float* tail_out,
@@ -1462,8 +1538,8 @@ alr_status alr_debug_decode_plan(const alr_config* cfg, int32_t n_cu, int32_t n_
 }
 
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
-                          int32_t N, int32_t K, int32_t tile, void* scratch, size_t scratch_bytes,
-                          alr_stream stream) {
+                          int32_t N, int32_t K, int32_t tile, void* splitk_scratch,
+                          size_t scratch_bytes, alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
   if (tile < 0 || (tile > 5 && tile < 17) || tile > 19) return ALR_E_INVALID_ARG;
@@ -1478,8 +1554,8 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   if (dtype == ALR_BF16) {
     const bf16* Wk = (const bf16*)W;
     if (tile == 18) {  // split-K: partial sums in the scratch buffer
-      if (!scratch || scratch_bytes < (size_t)2 * M * N * 4) return ALR_E_WORKSPACE;
-      dummy.splitk_buf = static_cast<float*>(scratch);
+      if (!splitk_scratch || scratch_bytes < (size_t)2 * M * N * 4) return ALR_E_WORKSPACE;
+      dummy.splitk_buf = static_cast<float*>(splitk_scratch);
       dummy.splitk_bytes = scratch_bytes;
     }
     launch_gemm<0, bf16>(&dummy, (const bf16*)A, K, Wk, K, M, N, K, el, s, tile);

@@ -1,0 +1,69 @@
+"""The no-allocation rollout entry point (alr_rollout_topk_noalloc) through the C ABI.
+
+It must give exactly what alr_rollout_topk gives without full log-probs (the same
+kernels on the same inputs; only where the per-step logit rows and partials live
+differs), on two calls in a row with the second one smaller, and refuse requests
+whose scratch would not fit the fixed array before anything is enqueued.
+"""
+import numpy as np
+import pytest
+
+from paper_2609_38795_amd import binding, workloads as W
+from gpu_util import make_engine, prefill
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _case(dtype):
+    base = W.get("small_bf16")
+    w = W.scaled(base, f"noalloc_{dtype}", n_layers=2, feat_layers=(0, 1), n_seq=2, seq_len=600,
+                 anchors_per_seq=20, anchor_lo=100, anchor_hi=590, block=8, dtype=dtype,
+                 d_model=256, n_heads=8, n_kv_heads=2, head_dim=32 if dtype == "f32" else 128,
+                 d_ffn=512)
+    return W.Inputs(w, W.random_weights(w.shape, 404, scale=0.05, norm_gain="random"),
+                    W.random_tokens(w.shape.vocab, (2, 600), 405, dist="zipf"),
+                    *W.random_anchors(2, 600, 20, 100, 590, 406), None, None)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_noalloc_equals_workspace_rollout_topk(dtype):
+    inp = _case(dtype)
+    w = inp.workload
+    V, B = w.shape.vocab, w.block
+    print(f"no-alloc rollout, {dtype}: vocab {V}, {w.n_anchors} then 7 anchors x {B} slots",
+          flush=True)
+    eng = make_engine(inp)
+    prefill(eng, inp)
+    dev = eng.device
+    for sel in (np.arange(w.n_anchors), np.array([3, 0, 17, 9, 30, 21, 39])):  # second call smaller
+        a_s, a_p = inp.anchor_seq[sel], inp.anchor_pos[sel]
+        n = len(sel)
+        ref = eng.rollout_topk(a_s, a_p, B)
+        out = (torch.full((n, B), -7, dtype=torch.int32, device=dev),
+               torch.full((n, B, 8), -7, dtype=torch.int32, device=dev),
+               torch.full((n, B, 8), 7.0, dtype=torch.float32, device=dev),
+               torch.full((n, B), 7.0, dtype=torch.float32, device=dev),
+               torch.full((n, B, w.shape.n_feat, w.shape.d_model), 7.0, dtype=torch.float32,
+                          device=dev))
+        got = eng.rollout_topk_noalloc(a_s, a_p, B, out)
+        torch.cuda.synchronize()
+        r_tok, r_ids, r_tl, r_tt, _, r_ft = ref
+        g_tok, g_ids, g_tl, g_tt, g_ft = got
+        assert torch.equal(g_tok, r_tok)
+        assert torch.equal(g_ids, r_ids)
+        assert torch.equal(g_tl, r_tl)
+        assert torch.equal(g_tt, r_tt)
+        assert torch.equal(g_ft, r_ft)
+        assert bool((g_ids[..., 0] == g_tok).all())
+        print(f"  {n} anchors: tokens, top-8 ids and log-probs, tails and features bit-identical",
+              flush=True)
+    # a request whose logit rows would not fit the fixed array is refused up front
+    per_row = V * 4 + (V // 64) * 12
+    n_big = (64 << 20) // per_row + 1
+    big = np.arange(n_big) % w.n_anchors
+    with pytest.raises(binding.AlrError) as ei:
+        eng.rollout_topk_noalloc(inp.anchor_seq[big], inp.anchor_pos[big], B, out)
+    assert ei.value.status == 3 and "no-alloc scratch" in str(ei.value)
+    eng.close()
