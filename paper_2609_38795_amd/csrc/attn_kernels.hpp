@@ -111,11 +111,13 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 // each 16-key group, so each V^T operand is one 16-byte LDS read.
 //
 // The shared V cache is stored transposed, [G][hd][column] per layer, with
-// every sequence's columns starting at a multiple of 64, so a 64-key V^T tile
-// is 16-byte loads of contiguous keys.  K tiles are [key][hd].  Both tiles are
+// every sequence's columns starting at a multiple of 64 and each aligned group
+// of 16 keys already in that lane-half order (vt_perm), so a 64-key V^T tile is
+// copied as contiguous 16-byte chunks.  K tiles are [key][hd].  Both tiles are
 // XOR-swizzled in 16-byte chunks so the MFMA operand reads are free of LDS
-// bank conflicts.  Tiles are double-buffered: the next tile's global loads are
-// in flight while the current one is consumed.
+// bank conflicts.  Tiles go from global memory straight into LDS
+// (attn_copy_tile) and are double-buffered: the next tile's copies are in
+// flight while the current one is consumed.
 
 constexpr int AT_KT = 64;
 // Decode split: the shared keys of every (anchor group, kv head) are cut into
@@ -142,71 +144,76 @@ struct AttnTile {
   bf16 vt[HD * AT_KT];  // [dim][key]
 };
 
-template <int HD>
-struct AttnStage {
-  u32x4 k[HD / 32];
-  u32x4 v[HD / 32];
-};
-
-// Global loads of one tile: keys k0..k0+63 of a sequence whose key 0 is token
-// row krow0 of the K cache and column vcol0 of the V^T cache.  Keys beyond
-// max_key read a clamped K row (they are masked anyway); their V entries are
-// zeroed when the tile is written to LDS (attn_lstore), which keeps unwritten
-// padding out of the sums without waiting for the loads here.
-template <int HD>
-__device__ __forceinline__ void attn_gload(AttnStage<HD>& st, const bf16* __restrict__ Kc,
-                                           long kv_rs, int kvh, long krow0,
-                                           const bf16* __restrict__ vT, long vt_stride,
-                                           long vcol0, int k0, int max_key) {
-  constexpr int NCHK = HD / 8;
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < HD / 32; ++i) {
-    const int ch = tid + 256 * i, key = ch / NCHK, c = ch % NCHK;
-    st.k[i] = *(const u32x4*)(Kc + (krow0 + min(k0 + key, max_key)) * kv_rs + (long)kvh * HD + c * 8);
-  }
-#pragma unroll
-  for (int i = 0; i < HD / 32; ++i) {
-    const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
-    st.v[i] = *(const u32x4*)(vT + (long)(kvh * HD + dim) * vt_stride + vcol0 + k0 + c * 8);
-  }
+__device__ __forceinline__ uint32_t lds_byte_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// LDS store of one tile; V entries of keys k0 + j > max_key are zeroed.
-template <int HD>
-__device__ __forceinline__ void attn_lstore(const AttnStage<HD>& st, AttnTile<HD>& t, int k0,
-                                            int max_key) {
-  constexpr int NCHK = HD / 8;
-  const int tid = threadIdx.x;
+// One wave-wide 1 KB copy global -> LDS (global_load_lds_dwordx4): lane i
+// fetches 16 bytes at gbase + voff and writes them to LDS byte m0 + 16 i.  No
+// VGPR holds the data and no ds_write is issued.  The compiler does not see the
+// copy, so every wait on it is explicit (attn_wait_copies).
+// m0 is named as clobbered for the reader; the compiler reserves it and uses
+// it in these kernels only for such copies (checked in their assembly).
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy_1k(uint32_t m0, uint32_t voff, const void* gbase) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(m0), "v"(voff), "s"(gbase)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(0) with the other counters left alone: this wave's copies
+// (and any earlier global loads) have landed.
+__device__ __forceinline__ void attn_wait_copies() {
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
+}
+
+// Makes the loads of v complete here: the compiler waits for them before this
+// point.  The tile copies are invisible to its wait counting, so a load left
+// outstanding into the loop would make its first use there wait for every
+// copy issued since as well (vmcnt counts both, in issue order).
+template <int N>
+__device__ __forceinline__ void attn_hold_loaded(const u32x4 (&v)[N]) {
 #pragma unroll
-  for (int i = 0; i < HD / 32; ++i) {
-    const int ch = tid + 256 * i, key = ch / NCHK, c = ch % NCHK;
-    *(u32x4*)(t.k + key * HD + chunk_swz<NCHK>(key, c) * 8) = st.k[i];
+  for (int i = 0; i < N; ++i) asm volatile("" : : "v"(v[i]));
+}
+
+// Copy of one 64-key tile into t by the workgroup's 4 waves: keys k0..k0+63
+// of a sequence whose key 0 is token row krow0 of the K cache and column vcol0
+// of the V^T cache.  Keys beyond max_key fetch K row max_key (they are masked
+// anyway); the V^T cache already holds its keys in the value MFMA's order
+// (vt_perm) and zeros in the columns that pad a sequence to a multiple of 64.
+// Each operand is HD/8 wave-wide 1 KB copies; copy j*4 + w belongs to wave w,
+// and lane l of it fills LDS chunk p = (j*4 + w)*64 + l of the operand's
+// XOR-swizzled layout, i.e. it fetches the global chunk the swizzle maps there.
+// Byte offsets from the layer's cache base fit 32 bits (checked on the host).
+template <int HD>
+__device__ __forceinline__ void attn_copy_tile(AttnTile<HD>& t, const bf16* __restrict__ Kc,
+                                               long kv_rs, int kvh, long krow0,
+                                               const bf16* __restrict__ vT, long vt_stride,
+                                               long vcol0, int k0, int max_key) {
+  constexpr int NCHK = HD / 8;
+  constexpr int NX = HD / 32;  // copies per wave per operand
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t kb = lds_byte_addr(t.k), vb = lds_byte_addr(t.vt);
+#pragma unroll
+  for (int j = 0; j < NX; ++j) {
+    const int blk = j * 4 + wave;
+    const int p = blk * 64 + lane, key = p / NCHK, c = chunk_swz<NCHK>(key, p % NCHK);
+    const uint32_t off =
+        (uint32_t)(((krow0 + min(k0 + key, max_key)) * kv_rs + (long)kvh * HD + c * 8) * 2);
+    copy_1k(kb + blk * 1024, off, Kc);
   }
 #pragma unroll
-  for (int i = 0; i < HD / 32; ++i) {
-    const int ch = tid + 256 * i, dim = ch >> 3, c = ch & 7;
-    const int g = c >> 1, q = c & 1;  // 16-key group, which half of it
-    u32x4 v = st.v[i];
-    const int kf = k0 + c * 8;
-    if (kf + 7 > max_key) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int ka = kf + 2 * e;
-        uint32_t w = v[e];
-        if (ka > max_key) w &= 0xFFFF0000u;
-        if (ka + 1 > max_key) w &= 0x0000FFFFu;
-        v[e] = w;
-      }
-    }
-    // keys 8c..8c+3 -> chunk 2g (half q); keys 8c+4..8c+7 -> chunk 2g+1 (half q)
-    u32x2 lo, hi;
-    lo[0] = v[0];
-    lo[1] = v[1];
-    hi[0] = v[2];
-    hi[1] = v[3];
-    *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g) * 8 + q * 4) = lo;
-    *(u32x2*)(t.vt + dim * AT_KT + chunk_swz<8>(dim, 2 * g + 1) * 8 + q * 4) = hi;
+  for (int j = 0; j < NX; ++j) {
+    const int blk = j * 4 + wave;
+    const int p = blk * 64 + lane, dim = p >> 3, c = chunk_swz<8>(dim, p & 7);
+    const uint32_t off =
+        (uint32_t)((((long)kvh * HD + dim) * vt_stride + vcol0 + k0 + c * 8) * 2);
+    copy_1k(vb + blk * 1024, off, vT);
   }
 }
 
@@ -337,8 +344,12 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
   bf16x8 qbv[HD / 16];
   {
     const bf16* qp = Q + (long)(w.start + q_row) * g.H * HD + (long)head * HD + h * 8;
+    u32x4 qraw[HD / 16];
 #pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks) qbv[ks] = as_bf16x8(*(const u32x4*)(qp + ks * 16));
+    for (int ks = 0; ks < HD / 16; ++ks) qraw[ks] = *(const u32x4*)(qp + ks * 16);
+    attn_hold_loaded<HD / 16>(qraw);
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks) qbv[ks] = as_bf16x8(qraw[ks]);
   }
   f32x16 o[HD / 32];
 #pragma unroll
@@ -348,21 +359,22 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
   float m = -INFINITY, l = 0.f;
   const int wave_last_q = min(qb * 32 + 31, w.len - 1);
   const int nt = wg_last_q / AT_KT + 1;
-  AttnStage<HD> st;
-  attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, 0, w.len - 1);
-  attn_lstore<HD>(st, tiles[0], 0, w.len - 1);
+  attn_copy_tile<HD>(tiles[0], Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, 0, w.len - 1);
+  attn_wait_copies();
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = it * AT_KT;
+    // the next tile streams into the other buffer while this one is consumed
     if (it + 1 < nt)
-      attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, k0 + AT_KT, w.len - 1);
+      attn_copy_tile<HD>(tiles[(it + 1) & 1], Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol,
+                         k0 + AT_KT, w.len - 1);
     if (active && k0 <= wave_last_q) {
       if (k0 + AT_KT - 1 > qb * 32)  // some key of the tile lies beyond some query: mask
         attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
       else
         attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
     }
-    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1], k0 + AT_KT, w.len - 1);
+    attn_wait_copies();
     __syncthreads();
   }
   if (active && q_pos < w.len)
@@ -372,8 +384,9 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
 // Decode work item: a group of up to 128/rep consecutive sorted anchors of one
 // sequence, one kv head, and the shared keys [kbeg, kend) of that sequence.
 // The item writes, per row (anchor-major, then head within the group), the
-// partial softmax state over those keys: running max m and sum l (log2
-// domain) and the unnormalised output.  attn_decode_combine_kernel merges the
+// partial softmax state over those keys: the reference max m (log2 domain; -inf
+// when none of the keys is visible to the row), the sum l of the weights, and the
+// output normalised by l, in fp16.  attn_decode_combine_kernel merges the
 // items of a group and adds the anchors' private rollout keys.  An item with
 // count = 0 is padding and does nothing.
 struct DecodeItem {
@@ -384,7 +397,7 @@ template <int HD>
 __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     const bf16* __restrict__ Q, const bf16* __restrict__ Kc, const bf16* __restrict__ vT,
     long vt_stride, const int* __restrict__ apos, const DecodeItem* __restrict__ work,
-    float* __restrict__ part_o, float* __restrict__ part_ml, AttnGeom g) {
+    uint16_t* __restrict__ part_o, float* __restrict__ part_ml, AttnGeom g) {
   __shared__ AttnTile<HD> tiles[2];
   const DecodeItem w = work[blockIdx.x];
   if (w.count == 0) return;  // uniform over the workgroup
@@ -400,8 +413,12 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
   bf16x8 qbv[HD / 16];
   {
     const bf16* qp = Q + (long)arow * g.H * HD + (long)head * HD + h * 8;
+    u32x4 qraw[HD / 16];
 #pragma unroll
-    for (int ks = 0; ks < HD / 16; ++ks) qbv[ks] = as_bf16x8(*(const u32x4*)(qp + ks * 16));
+    for (int ks = 0; ks < HD / 16; ++ks) qraw[ks] = *(const u32x4*)(qp + ks * 16);
+    attn_hold_loaded<HD / 16>(qraw);
+#pragma unroll
+    for (int ks = 0; ks < HD / 16; ++ks) qbv[ks] = as_bf16x8(qraw[ks]);
   }
   f32x16 o[HD / 32];
 #pragma unroll
@@ -416,40 +433,41 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     wave_min = min(wave_min, __shfl_xor(wave_min, off));
   }
   const int nt = (w.kend - w.kbeg + AT_KT - 1) / AT_KT;
-  AttnStage<HD> st;
-  attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg, w.kend - 1);
-  attn_lstore<HD>(st, tiles[0], w.kbeg, w.kend - 1);
+  attn_copy_tile<HD>(tiles[0], Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg,
+                     w.kend - 1);
+  attn_wait_copies();
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = w.kbeg + it * AT_KT;
     if (it + 1 < nt)
-      attn_gload<HD>(st, Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, k0 + AT_KT,
-                     w.kend - 1);
+      attn_copy_tile<HD>(tiles[(it + 1) & 1], Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0,
+                         k0 + AT_KT, w.kend - 1);
     if (k0 <= wave_lim) {
       if (k0 + AT_KT - 1 > wave_min)
         attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
       else
         attn_tile_update<HD, false>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
     }
-    if (it + 1 < nt) attn_lstore<HD>(st, tiles[(it + 1) & 1], k0 + AT_KT, w.kend - 1);
+    attn_wait_copies();
     __syncthreads();
   }
   if (!active) return;
+  // the chunk's output normalised by its own sum, in fp16 (a convex combination
+  // of value rows: no range issue), zeros when no key of the chunk is visible
   const long prow = (long)w.part * 128 + rho;
-  float* po = part_o + prow * HD;
+  uint16_t* po = part_o + prow * HD;
+  const float inv = (l > 0.f) ? 1.f / l : 0.f;
 #pragma unroll
   for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      f32x4 v;
-      v[0] = o[db][4 * i];
-      v[1] = o[db][4 * i + 1];
-      v[2] = o[db][4 * i + 2];
-      v[3] = o[db][4 * i + 3];
-      *(f32x4*)(po + db * 32 + 8 * i + 4 * h) = v;
+      u32x2 v;
+      v[0] = pack2h(o[db][4 * i] * inv, o[db][4 * i + 1] * inv);
+      v[1] = pack2h(o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
+      *(u32x2*)(po + db * 32 + 8 * i + 4 * h) = v;
     }
   if (h == 0) {
-    part_ml[prow * 2] = m * g.scale_log2;  // log2 domain for the combine
+    part_ml[prow * 2] = (l > 0.f) ? m * g.scale_log2 : -INFINITY;  // log2 domain
     part_ml[prow * 2 + 1] = l;
   }
 }
@@ -461,7 +479,7 @@ struct DecodeGroup {
 
 // One wave per (sorted anchor r, kv head): for each query head j of the kv
 // head's group it merges the chunk partials of the shared keys (log2-domain
-// max m, sum l, unnormalised output) and then the anchor's private rollout
+// reference m, sum l, output normalised by l in fp16) and then the anchor's private rollout
 // keys 1..n_priv (one softmax over both), and writes the attention output.
 // A head is handled by HD/8 lanes with 8 dimensions each, so one pass covers
 // 64/(HD/8) heads and a score is a reduction over those lanes.  The private
@@ -469,7 +487,7 @@ struct DecodeGroup {
 template <int HD>
 __global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
     const int* __restrict__ grp_of_row, const DecodeGroup* __restrict__ groups,
-    const float* __restrict__ part_o, const float* __restrict__ part_ml,
+    const uint16_t* __restrict__ part_o, const float* __restrict__ part_ml,
     const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     long priv_rs, int n_priv, bf16* __restrict__ O, int n_rows, AttnGeom g) {
   constexpr int LPH = HD / 8;    // lanes per head
@@ -516,14 +534,13 @@ __global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
     for (int c = 0; c < grp.nchunk; ++c) {
       const long prow = p0 + (long)c * 128;
       const float mc = part_ml[prow * 2];
-      const float a = (mc == -INFINITY) ? 0.f : fast_exp2(mc - mt);
-      lt = fmaf(part_ml[prow * 2 + 1], a, lt);
-      const f32x4 o0 = *(const f32x4*)(part_o + prow * HD + dl * 8);
-      const f32x4 o1 = *(const f32x4*)(part_o + prow * HD + dl * 8 + 4);
+      const float wgt = (mc == -INFINITY) ? 0.f : part_ml[prow * 2 + 1] * fast_exp2(mc - mt);
+      lt += wgt;
+      const u32x4 ow = *(const u32x4*)(part_o + prow * HD + dl * 8);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        acc[e] = fmaf(o0[e], a, acc[e]);
-        acc[4 + e] = fmaf(o1[e], a, acc[4 + e]);
+        acc[2 * e] = fmaf(wgt, h_lo(ow[e]), acc[2 * e]);
+        acc[2 * e + 1] = fmaf(wgt, h_hi(ow[e]), acc[2 * e + 1]);
       }
     }
     // private keys, in blocks of PB: all key and value rows of a block are

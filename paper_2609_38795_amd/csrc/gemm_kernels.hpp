@@ -19,6 +19,15 @@ namespace alr {
 
 // ------------------------------------------------------------------ epilogues
 
+// Column order of the transposed V cache inside every aligned group of 16
+// keys: keys 0-3, 8-11, 4-7, 12-15 (the second and third runs of four swap).
+// That is the order in which the attention kernels' value MFMA consumes a
+// 16-key step (lane half h supplies keys 4h..4h+3 and 8+4h..8+4h+3), so a tile
+// goes from global memory to LDS unchanged.  The map is its own inverse.
+__device__ __forceinline__ int vt_perm(int col) {
+  return col ^ ((((col >> 2) ^ (col >> 3)) & 1) * 12);
+}
+
 // QKV projection + RoPE + key/value store.  Columns [0, H*hd) are q, then
 // [H*hd, H*hd+G*hd) k, then v.  In the q and k sections, 64-column group t
 // holds, in its low half, entries f = 32t .. 32t+31 of the list of
@@ -30,7 +39,7 @@ struct EpiQKV {
   OutT* k;            // row r -> k + r*kv_rs
   OutT* v;            // row r -> v + r*kv_rs (when vt_col is null)
   long kv_rs;
-  const int* vt_col;  // if set: v is transposed, element (row, c) at v[c*vt_stride + vt_col[row]]
+  const int* vt_col;  // if set: v is transposed, element (row, c) at v[c*vt_stride + vt_perm(vt_col[row])]
   long vt_stride;
   const float* cosT;  // [max_pos, hd/2]
   const float* sinT;
@@ -59,7 +68,7 @@ struct EpiQKV {
       Elt<OutT>::st(dst + head * hd + i, lo * cs - hi * sn);
       Elt<OutT>::st(dst + head * hd + i + half, hi * cs + lo * sn);
     } else if (vt_col) {
-      const long cl = c - qd - kd, col = vt_col[row];
+      const long cl = c - qd - kd, col = vt_perm(vt_col[row]);
       Elt<OutT>::st(v + cl * vt_stride + col, lo);
       Elt<OutT>::st(v + (cl + 32) * vt_stride + col, hi);
     } else {
@@ -130,16 +139,17 @@ struct EpiQKV {
             wl[1] = pack2bf(lo[t0 + 2], lo[t0 + 3]);
             wh[0] = pack2bf(hi[t0], hi[t0 + 1]);
             wh[1] = pack2bf(hi[t0 + 2], hi[t0 + 3]);
-            *(u32x2*)(v + cl * vt_stride + col[t0]) = wl;
-            *(u32x2*)(v + (cl + 32) * vt_stride + col[t0]) = wh;
+            const int pc = vt_perm(col[t0]);  // a 4-aligned run of 4 stays together
+            *(u32x2*)(v + cl * vt_stride + pc) = wl;
+            *(u32x2*)(v + (cl + 32) * vt_stride + pc) = wh;
             continue;
           }
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           if (r[t0 + e] < M) {
-            Elt<OutT>::st(v + cl * vt_stride + col[t0 + e], lo[t0 + e]);
-            Elt<OutT>::st(v + (cl + 32) * vt_stride + col[t0 + e], hi[t0 + e]);
+            Elt<OutT>::st(v + cl * vt_stride + vt_perm(col[t0 + e]), lo[t0 + e]);
+            Elt<OutT>::st(v + (cl + 32) * vt_stride + vt_perm(col[t0 + e]), hi[t0 + e]);
           }
       }
     } else {

@@ -386,6 +386,26 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
 }
 
+// Zero the entries of the transposed V cache that pad each sequence to a
+// multiple of 64 keys: attention tiles copy them into LDS, and their
+// probabilities being 0 keeps them out of the sums only if they hold finite
+// values.  pad[2 s] is sequence s's first padding key column, pad[2 s + 1] the
+// number of padding keys (< 64); key column k is stored at vt_perm(k).  Thread
+// t covers sequence t % n_seq, cache row (t / n_seq) % rows, layer t / (n_seq rows).
+__global__ __launch_bounds__(256) void zero_vt_pad_kernel(bf16* __restrict__ vc,
+                                                          long layer_elems, long vt_stride,
+                                                          const int* __restrict__ pad, int n_seq,
+                                                          int rows, long total) {
+  const long t = (long)blockIdx.x * 256 + threadIdx.x;
+  if (t >= total) return;
+  const int sq = (int)(t % n_seq);
+  const long rl = t / n_seq;
+  const int row = (int)(rl % rows);
+  const long layer = rl / rows;
+  bf16* p = vc + layer * layer_elems + (long)row * vt_stride;
+  for (int c = 0; c < pad[2 * sq + 1]; ++c) p[vt_perm(pad[2 * sq] + c)] = 0;
+}
+
 // Corpus-label rows of slot s: row r takes the prefill's final-norm row at
 // position min(a + s, len - 1) of its sequence (a = apos[r], len = alen[r],
 // first token row atok[r] - apos[r]); valid[r] = (a + s <= len - 1);

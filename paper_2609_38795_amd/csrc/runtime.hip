@@ -55,7 +55,7 @@ struct Layout {
   size_t resid, xnorm, qbuf, attn, act;
   size_t i_tokpos, i_rowstart, i_perm, i_apos, i_rpos, i_atok, i_aseq, i_alen, i_cur;
   size_t i_valid, i_target, i_ira, i_ctok, logits, lm_part;
-  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_groups, i_grprow, i_rowptr;
+  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_vtpad, i_groups, i_grprow, i_rowptr;
   size_t part_o, part_ml;
   size_t splitk, splitk_bytes;
   size_t max_pwork, max_dwork, max_groups;
@@ -146,6 +146,12 @@ alr_status check_operand_sizes(const alr_config& c, const alr_limits& lim, char*
   if (wmax >= lim32)
     return fmt_msg(msg, len, "a weight matrix of the config is >= 4 GiB in bf16"),
            ALR_E_UNSUPPORTED;
+  // the attention kernels copy key/value tiles by 32-bit byte offsets into one
+  // layer's cache (tokens, or transposed-V columns with per-sequence padding)
+  const double vt_cols = std::ceil((lim.max_tokens + 64.0 * lim.max_seqs) / 64.0) * 64.0;
+  if (std::max((double)lim.max_tokens, vt_cols) * kvd * 2.0 >= lim32)
+    return fmt_msg(msg, len, "one layer's key/value cache is >= 4 GiB (lower max_tokens)"),
+           ALR_E_UNSUPPORTED;
   return ALR_OK;
 }
 
@@ -234,9 +240,10 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_maps = take(((qd + 2 * kvd) + 2 * F) * 4);
   L.i_rowptr = take(std::max((size_t)c.vocab, qd + 2 * kvd + 2 * d + 2 * F) * sizeof(void*));
   L.i_vtcol = take(T * 4);
+  L.i_vtpad = take((size_t)lim.max_seqs * 2 * 4);
   L.i_groups = take(L.max_groups * sizeof(DecodeGroup));
   L.i_grprow = take(NA * 4);
-  L.part_o = take(L.max_dwork * 128 * hd * 4);
+  L.part_o = take(L.max_dwork * 128 * hd * 2);  // fp16, normalised by the chunk sum
   L.part_ml = take(L.max_dwork * 128 * 2 * 4);
   // split-K partial sums of the rollout GEMMs: up to 4 slices of [anchors, N] fp32
   L.splitk_bytes = 4 * NA * std::max(qd + 2 * kvd, d) * 4;
@@ -309,7 +316,7 @@ struct alr_ctx {
   size_t splitk_bytes = 0;
   int n_seq = 0;
   std::vector<int> seq_len, seq_off;
-  std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol;
+  std::vector<int> h_tokpos, h_rowstart, h_vtcol, seq_vcol, h_vtpad;
   std::vector<PrefillItem> h_pwork;
   std::vector<int> h_anch;  // perm | apos | atok | aseq | alen (n each) | rope positions (3n)
   std::vector<int> h_ira;   // secondary primaries | offsets
@@ -582,7 +589,7 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
     if (mfma_attn(c)) {
       const int nw = (int)ctx->h_dwork.size();
       const DecodeItem* wk = ctx->at<DecodeItem>(L.i_dwork);
-      float* po = ctx->at<float>(L.part_o);
+      uint16_t* po = ctx->at<uint16_t>(L.part_o);
       float* pml = ctx->at<float>(L.part_ml);
       const unsigned ncomb = (unsigned)(((long)M * G + 3) / 4);
       const int* grow = ctx->at<int>(L.i_grprow);
@@ -664,6 +671,18 @@ alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* 
                                      reinterpret_cast<const T*>(embeds), mask, d);
   keep_tokens_kernel<<<(M + 255) / 256, 256, 0, st>>>(ctx->at<int>(L.i_ctok), tokens, mask, M);
   ALR_LAUNCHED(ctx, "embed");
+  if constexpr (std::is_same<T, bf16>::value) {
+    bool any_pad = false;
+    for (int i = 0; i < ctx->n_seq; ++i) any_pad |= ctx->h_vtpad[2 * i + 1] > 0;
+    if (L.vt_stride && any_pad && c.n_layers > 0) {
+      const int rows = c.n_kv_heads * c.head_dim;
+      const long total = (long)c.n_layers * rows * ctx->n_seq;
+      zero_vt_pad_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+          reinterpret_cast<bf16*>(ctx->ws + L.vc), (long)(L.kv_layer_stride / 2),
+          (long)L.vt_stride, ctx->at<int>(L.i_vtpad), ctx->n_seq, rows, total);
+      ALR_LAUNCHED(ctx, "transposed-V padding");
+    }
+  }
   for (int l = 0; l < c.n_layers; ++l) {
     const int f = feat_index(c, l);
     float* feat = f >= 0 ? ctx->at<float>(L.feat_store) + (long)f * d : nullptr;
@@ -1087,6 +1106,11 @@ alr_status alr_prefill_positions(alr_ctx* ctx, int32_t n_seq, const int32_t* seq
       for (int it = 0; it < n_items; it += 4)
         ctx->h_pwork.push_back(PrefillItem{ctx->seq_off[i], ctx->seq_vcol[i], seq_len[i], g, it});
   }
+  ctx->h_vtpad.assign((size_t)2 * n_seq, 0);
+  for (int i = 0; i < n_seq; ++i) {
+    ctx->h_vtpad[2 * i] = ctx->seq_vcol[i] + seq_len[i];
+    ctx->h_vtpad[2 * i + 1] = (seq_len[i] + 63) / 64 * 64 - seq_len[i];
+  }
   // causal work grows with the query position: start the longest items first
   std::stable_sort(ctx->h_pwork.begin(), ctx->h_pwork.end(),
                    [rep](const PrefillItem& a, const PrefillItem& b) {
@@ -1098,6 +1122,8 @@ alr_status alr_prefill_positions(alr_ctx* ctx, int32_t n_seq, const int32_t* seq
   st = upload(ctx, ctx->at<int>(L.i_tokpos), ctx->h_tokpos.data(), (size_t)M * 3 * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_rowstart), ctx->h_rowstart.data(), (size_t)M * 4, s);
   if (st == ALR_OK) st = upload(ctx, ctx->at<int>(L.i_vtcol), ctx->h_vtcol.data(), (size_t)M * 4, s);
+  if (st == ALR_OK)
+    st = upload(ctx, ctx->at<int>(L.i_vtpad), ctx->h_vtpad.data(), (size_t)n_seq * 2 * 4, s);
   if (st == ALR_OK)
     st = upload(ctx, ctx->at<PrefillItem>(L.i_pwork), ctx->h_pwork.data(),
                 ctx->h_pwork.size() * sizeof(PrefillItem), s);
