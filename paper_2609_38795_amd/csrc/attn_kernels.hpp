@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(
 // copied as contiguous 16-byte chunks.  K tiles are [key][hd].  Both tiles are
 // XOR-swizzled in 16-byte chunks so the MFMA operand reads are free of LDS
 // bank conflicts.  Tiles go from global memory straight into LDS
-// (attn_copy_tile) and are double-buffered: the next tile's copies are in
+// (AttnCopier) and are double-buffered: the next tile's copies are in
 // flight while the current one is consumed.
 
 constexpr int AT_KT = 64;
@@ -180,7 +180,7 @@ __device__ __forceinline__ void attn_hold_loaded(const u32x4 (&v)[N]) {
   for (int i = 0; i < N; ++i) asm volatile("" : : "v"(v[i]));
 }
 
-// Copy of one 64-key tile into t by the workgroup's 4 waves: keys k0..k0+63
+// Copies of 64-key tiles into LDS by the workgroup's 4 waves, for keys k0..k0+63
 // of a sequence whose key 0 is token row krow0 of the K cache and column vcol0
 // of the V^T cache.  Keys beyond max_key fetch K row max_key (they are masked
 // anyway); the V^T cache already holds its keys in the value MFMA's order
@@ -188,34 +188,52 @@ __device__ __forceinline__ void attn_hold_loaded(const u32x4 (&v)[N]) {
 // Each operand is HD/8 wave-wide 1 KB copies; copy j*4 + w belongs to wave w,
 // and lane l of it fills LDS chunk p = (j*4 + w)*64 + l of the operand's
 // XOR-swizzled layout, i.e. it fetches the global chunk the swizzle maps there.
-// Byte offsets from the layer's cache base fit 32 bits (checked on the host).
+// The lane's part of each offset is formed once per work item; a tile adds
+// its first key (a row multiple for K, a column for V^T).  Byte offsets from
+// the layer's cache base fit 32 bits (checked on the host).
 template <int HD>
-__device__ __forceinline__ void attn_copy_tile(AttnTile<HD>& t, const bf16* __restrict__ Kc,
-                                               long kv_rs, int kvh, long krow0,
-                                               const bf16* __restrict__ vT, long vt_stride,
-                                               long vcol0, int k0, int max_key) {
-  constexpr int NCHK = HD / 8;
-  constexpr int NX = HD / 32;  // copies per wave per operand
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t kb = lds_byte_addr(t.k), vb = lds_byte_addr(t.vt);
+struct AttnCopier {
+  static constexpr int NCHK = HD / 8;
+  static constexpr int NX = HD / 32;  // copies per wave per operand
+  uint32_t koff[NX], voff[NX];        // byte offsets of the lane's chunks at k0 = 0
+  int key[NX];                        // the lane's key within the tile, per K copy
+  uint32_t krow_bytes;                // bytes of one K-cache row
+  int wave;
+
+  __device__ __forceinline__ AttnCopier(long kv_rs, int kvh, long krow0, long vt_stride,
+                                        long vcol0) {
+    const int lane = threadIdx.x & 63;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    krow_bytes = (uint32_t)(kv_rs * 2);
 #pragma unroll
-  for (int j = 0; j < NX; ++j) {
-    const int blk = j * 4 + wave;
-    const int p = blk * 64 + lane, key = p / NCHK, c = chunk_swz<NCHK>(key, p % NCHK);
-    const uint32_t off =
-        (uint32_t)(((krow0 + min(k0 + key, max_key)) * kv_rs + (long)kvh * HD + c * 8) * 2);
-    copy_1k(kb + blk * 1024, off, Kc);
+    for (int j = 0; j < NX; ++j) {
+      const int p = (j * 4 + wave) * 64 + lane;
+      key[j] = p / NCHK;
+      const int ck = chunk_swz<NCHK>(key[j], p % NCHK);
+      koff[j] = (uint32_t)((krow0 * kv_rs + (long)kvh * HD + ck * 8) * 2);
+      const int dim = p >> 3, cv = chunk_swz<8>(dim, p & 7);
+      voff[j] = (uint32_t)((((long)kvh * HD + dim) * vt_stride + vcol0 + cv * 8) * 2);
+    }
   }
+
+  __device__ __forceinline__ void tile(AttnTile<HD>& t, const bf16* __restrict__ Kc,
+                                       const bf16* __restrict__ vT, int k0, int max_key) const {
+    const uint32_t kb = lds_byte_addr(t.k), vb = lds_byte_addr(t.vt);
+    if (k0 + AT_KT - 1 <= max_key) {  // uniform: no key of the tile past max_key
 #pragma unroll
-  for (int j = 0; j < NX; ++j) {
-    const int blk = j * 4 + wave;
-    const int p = blk * 64 + lane, dim = p >> 3, c = chunk_swz<8>(dim, p & 7);
-    const uint32_t off =
-        (uint32_t)((((long)kvh * HD + dim) * vt_stride + vcol0 + k0 + c * 8) * 2);
-    copy_1k(vb + blk * 1024, off, vT);
+      for (int j = 0; j < NX; ++j)
+        copy_1k(kb + (j * 4 + wave) * 1024, koff[j] + (uint32_t)(k0 + key[j]) * krow_bytes, Kc);
+    } else {
+#pragma unroll
+      for (int j = 0; j < NX; ++j)
+        copy_1k(kb + (j * 4 + wave) * 1024,
+                koff[j] + (uint32_t)min(k0 + key[j], max_key) * krow_bytes, Kc);
+    }
+#pragma unroll
+    for (int j = 0; j < NX; ++j)
+      copy_1k(vb + (j * 4 + wave) * 1024, voff[j] + (uint32_t)k0 * 2, vT);
   }
-}
+};
 
 // One 64-key tile of the online softmax for the wave's 32 queries.
 //   qb[ks]: Q^T operand (lane: query lane&31, dims 8*(lane>>5) + 16 ks .. +7)
@@ -359,15 +377,14 @@ __global__ __launch_bounds__(256, 2) void attn_prefill_mfma_kernel(
   float m = -INFINITY, l = 0.f;
   const int wave_last_q = min(qb * 32 + 31, w.len - 1);
   const int nt = wg_last_q / AT_KT + 1;
-  attn_copy_tile<HD>(tiles[0], Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol, 0, w.len - 1);
+  const AttnCopier<HD> cp(kv_rs, w.kvh, w.start, vt_stride, w.vcol);
+  cp.tile(tiles[0], Kc, vT, 0, w.len - 1);
   attn_wait_copies();
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = it * AT_KT;
     // the next tile streams into the other buffer while this one is consumed
-    if (it + 1 < nt)
-      attn_copy_tile<HD>(tiles[(it + 1) & 1], Kc, kv_rs, w.kvh, w.start, vT, vt_stride, w.vcol,
-                         k0 + AT_KT, w.len - 1);
+    if (it + 1 < nt) cp.tile(tiles[(it + 1) & 1], Kc, vT, k0 + AT_KT, w.len - 1);
     if (active && k0 <= wave_last_q) {
       if (k0 + AT_KT - 1 > qb * 32)  // some key of the tile lies beyond some query: mask
         attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, q_pos, g.scale_log2);
@@ -433,15 +450,13 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
     wave_min = min(wave_min, __shfl_xor(wave_min, off));
   }
   const int nt = (w.kend - w.kbeg + AT_KT - 1) / AT_KT;
-  attn_copy_tile<HD>(tiles[0], Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0, w.kbeg,
-                     w.kend - 1);
+  const AttnCopier<HD> cp(kv_rs, w.kvh, w.krow0, vt_stride, w.vcol0);
+  cp.tile(tiles[0], Kc, vT, w.kbeg, w.kend - 1);
   attn_wait_copies();
   __syncthreads();
   for (int it = 0; it < nt; ++it) {
     const int k0 = w.kbeg + it * AT_KT;
-    if (it + 1 < nt)
-      attn_copy_tile<HD>(tiles[(it + 1) & 1], Kc, kv_rs, w.kvh, w.krow0, vT, vt_stride, w.vcol0,
-                         k0 + AT_KT, w.kend - 1);
+    if (it + 1 < nt) cp.tile(tiles[(it + 1) & 1], Kc, vT, k0 + AT_KT, w.kend - 1);
     if (k0 <= wave_lim) {
       if (k0 + AT_KT - 1 > wave_min)
         attn_tile_update<HD, true>(tiles[it & 1], qbv, o, m, l, k0, lim, g.scale_log2);
