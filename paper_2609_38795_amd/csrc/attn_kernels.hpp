@@ -487,7 +487,8 @@ __global__ __launch_bounds__(256, 2) void attn_decode_mfma_kernel(
   }
 }
 
-// Group of sorted anchors as the combine kernel sees it.
+// Group of sorted anchors as the planner sees it (the combine kernel reads, per
+// sorted row, its first partial row and the chunk count: the row table).
 struct DecodeGroup {
   int first, nchunk, part0;  // part index of (kv head 0, chunk 0); kv head g adds g*nchunk
 };
@@ -501,7 +502,7 @@ struct DecodeGroup {
 // key and value rows of the kv head are read by every head of the pass.
 template <int HD>
 __global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
-    const int* __restrict__ grp_of_row, const DecodeGroup* __restrict__ groups,
+    const int2* __restrict__ rowinfo,
     const uint16_t* __restrict__ part_o, const float* __restrict__ part_ml,
     const bf16* __restrict__ Q, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     long priv_rs, int n_priv, bf16* __restrict__ O, int n_rows, AttnGeom g) {
@@ -513,7 +514,9 @@ __global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
   if (item >= (long)n_rows * g.G) return;  // no barrier in this kernel
   const int r = (int)(item / g.G), kvh = (int)(item % g.G);
   const int rep = g.H / g.G;
-  const DecodeGroup grp = groups[grp_of_row[r]];
+  // (first partial row of the anchor at kv head 0 and chunk 0, chunks of its group)
+  const int2 ri = rowinfo[r];
+  const int nchunk = ri.y;
   const int hh = lane / LPH, dl = lane % LPH;
   const long kv_rs = (long)g.G * HD;
   const bf16* kp = Kp + (long)r * priv_rs + (long)kvh * HD + dl * 8;
@@ -533,30 +536,27 @@ __global__ __launch_bounds__(256, 4) void attn_decode_combine_kernel(
       }
     }
     // shared keys: merge the chunk partials
-    const int rho = (r - grp.first) * rep + jc;
-    const long p0 = (long)(grp.part0 + kvh * grp.nchunk) * 128 + rho;  // chunk c adds c*128
-    // chunk maxima: the LPH lanes of a head read LPH chunks at a time
-    float mt = -INFINITY;
-    for (int c0 = 0; c0 < grp.nchunk; c0 += LPH) {
-      const int c = c0 + dl;
-      mt = fmaxf(mt, c < grp.nchunk ? part_ml[(p0 + (long)c * 128) * 2] : -INFINITY);
-    }
-    mt = group_max<LPH>(mt);
-    float lt = 0.f, acc[8];
+    const long p0 = (long)ri.x + (long)kvh * nchunk * 128 + jc;  // chunk c adds c*128
+    // one online pass: all of a round's loads are independent of each other
+    float mt = -INFINITY, lt = 0.f, acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.f;
 #pragma unroll 4
-    for (int c = 0; c < grp.nchunk; ++c) {
+    for (int c = 0; c < nchunk; ++c) {
       const long prow = p0 + (long)c * 128;
-      const float mc = part_ml[prow * 2];
-      const float wgt = (mc == -INFINITY) ? 0.f : part_ml[prow * 2 + 1] * fast_exp2(mc - mt);
-      lt += wgt;
+      const f32x2 ml = *(const f32x2*)(part_ml + prow * 2);
+      const float mc = ml[0], lc = ml[1];
       const u32x4 ow = *(const u32x4*)(part_o + prow * HD + dl * 8);
+      const float mn = fmaxf(mt, mc);
+      const float alpha = (mt == -INFINITY) ? 0.f : fast_exp2(mt - mn);
+      const float wgt = (mc == -INFINITY) ? 0.f : lc * fast_exp2(mc - mn);
+      lt = fmaf(lt, alpha, wgt);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        acc[2 * e] = fmaf(wgt, h_lo(ow[e]), acc[2 * e]);
-        acc[2 * e + 1] = fmaf(wgt, h_hi(ow[e]), acc[2 * e + 1]);
+        acc[2 * e] = fmaf(acc[2 * e], alpha, wgt * h_lo(ow[e]));
+        acc[2 * e + 1] = fmaf(acc[2 * e + 1], alpha, wgt * h_hi(ow[e]));
       }
+      mt = mn;
     }
     // private keys, in blocks of PB: all key and value rows of a block are
     // loaded first (rows past n_priv re-read the last valid one), then the

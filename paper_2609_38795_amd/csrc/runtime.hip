@@ -55,7 +55,7 @@ struct Layout {
   size_t resid, xnorm, qbuf, attn, act;
   size_t i_tokpos, i_rowstart, i_perm, i_apos, i_rpos, i_atok, i_aseq, i_alen, i_cur;
   size_t i_valid, i_target, i_ira, i_ctok, logits, lm_part;
-  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_vtpad, i_groups, i_grprow, i_rowptr;
+  size_t i_pwork, i_dwork, i_maps, i_vtcol, i_vtpad, i_rowinfo, i_rowptr;
   size_t part_o, part_ml;
   size_t splitk, splitk_bytes;
   size_t max_pwork, max_dwork, max_groups;
@@ -241,8 +241,7 @@ size_t compute_layout(const alr_config& c, const alr_limits& lim, Layout& L) {
   L.i_rowptr = take(std::max((size_t)c.vocab, qd + 2 * kvd + 2 * d + 2 * F) * sizeof(void*));
   L.i_vtcol = take(T * 4);
   L.i_vtpad = take((size_t)lim.max_seqs * 2 * 4);
-  L.i_groups = take(L.max_groups * sizeof(DecodeGroup));
-  L.i_grprow = take(NA * 4);
+  L.i_rowinfo = take(NA * 2 * 4);
   L.part_o = take(L.max_dwork * 128 * hd * 2);  // fp16, normalised by the chunk sum
   L.part_ml = take(L.max_dwork * 128 * 2 * 4);
   // split-K partial sums of the rollout GEMMs: up to 4 slices of [anchors, N] fp32
@@ -322,7 +321,7 @@ struct alr_ctx {
   std::vector<int> h_ira;   // secondary primaries | offsets
   std::vector<DecodeItem> h_dwork;
   std::vector<DecodeGroup> h_groups;
-  std::vector<int> h_grprow;
+  std::vector<int> h_grprow, h_rowinfo;
   std::string err;
   // launch timing of one site (alr_profile_*)
   int prof_site = 0;
@@ -592,20 +591,19 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
       uint16_t* po = ctx->at<uint16_t>(L.part_o);
       float* pml = ctx->at<float>(L.part_ml);
       const unsigned ncomb = (unsigned)(((long)M * G + 3) / 4);
-      const int* grow = ctx->at<int>(L.i_grprow);
-      const DecodeGroup* grp = ctx->at<DecodeGroup>(L.i_groups);
+      const int2* rinfo = ctx->at<int2>(L.i_rowinfo);
       if constexpr (std::is_same<T, bf16>::value) {
         if (hd == 128) {
           attn_decode_mfma_kernel<128><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride,
                                                             ctx->at<int>(L.i_apos), wk, po, pml, g);
           ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
-          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, qb, kp, vp,
+          attn_decode_combine_kernel<128><<<ncomb, 256, 0, st>>>(rinfo, po, pml, qb, kp, vp,
                                                                  priv_rs, s, at, M, g);
         } else {
           attn_decode_mfma_kernel<64><<<nw, 256, 0, st>>>(qb, kc, vc, (long)L.vt_stride,
                                                            ctx->at<int>(L.i_apos), wk, po, pml, g);
           ProfScope pc(ctx, ALR_PROF_DECODE_COMBINE, st);
-          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(grow, grp, po, pml, qb, kp, vp,
+          attn_decode_combine_kernel<64><<<ncomb, 256, 0, st>>>(rinfo, po, pml, qb, kp, vp,
                                                                 priv_rs, s, at, M, g);
         }
       }
@@ -1321,6 +1319,16 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
                   ctx->seq_vcol.data(), ctx->h_dwork, ctx->h_groups, ctx->h_grprow);
     }
   }
+  // per sorted row: its first partial row (kv head 0, chunk 0) and its group's chunk count
+  ctx->h_rowinfo.assign((size_t)2 * n, 0);
+  if (!ctx->h_groups.empty()) {
+    const int rep_h = c.n_heads / c.n_kv_heads;
+    for (int r = 0; r < n; ++r) {
+      const DecodeGroup& dg = ctx->h_groups[ctx->h_grprow[r]];
+      ctx->h_rowinfo[2 * r] = dg.part0 * 128 + (r - dg.first) * rep_h;
+      ctx->h_rowinfo[2 * r + 1] = dg.nchunk;
+    }
+  }
   if (ctx->h_dwork.size() > ctx->L.max_dwork || ctx->h_groups.size() > ctx->L.max_groups)
     return fail(ctx, ALR_E_WORKSPACE, "decode work list overflow");
   const Layout& L = ctx->L;
@@ -1333,11 +1341,9 @@ alr_status prepare_anchors(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor
   if (st == ALR_OK && !ctx->h_dwork.empty())
     st = upload(ctx, ctx->at<DecodeItem>(L.i_dwork), ctx->h_dwork.data(),
                 ctx->h_dwork.size() * sizeof(DecodeItem), s);
-  if (st == ALR_OK && !ctx->h_groups.empty())
-    st = upload(ctx, ctx->at<DecodeGroup>(L.i_groups), ctx->h_groups.data(),
-                ctx->h_groups.size() * sizeof(DecodeGroup), s);
+
   if (st == ALR_OK && rollout)
-    st = upload(ctx, ctx->at<int>(L.i_grprow), ctx->h_grprow.data(), (size_t)n * 4, s);
+    st = upload(ctx, ctx->at<int>(L.i_rowinfo), ctx->h_rowinfo.data(), (size_t)n * 2 * 4, s);
   return st;
 }
 
