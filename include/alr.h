@@ -238,12 +238,12 @@ alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* ancho
  * the same arguments, checks and results as alr_rollout_topk with
  * logprobs_out = NULL, but the per-step scratch -- each step's fp32 logit rows
  * [n_anchor, vocab] and their per-64-column log-sum-exp partials [n_anchor,
- * vocab/64] of 12 bytes -- lives in a fixed array of ALR_NOALLOC_SCRATCH_BYTES
+ * vocab/64] of 8 bytes -- lives in a fixed array of ALR_NOALLOC_SCRATCH_BYTES
  * that the library holds on every device it runs on until the process ends
  * (its address is looked up once per device by alr_create), not in the
  * context's workspace.  The call allocates nothing and frees nothing.
- *   Limit: 256-byte-aligned n_anchor * vocab * 4 plus n_anchor * (vocab/64) * 12
- *   must fit in the array (e.g. 128 anchors at vocab 128256, 500 at 32000);
+ *   Limit: 256-byte-aligned n_anchor * vocab * 4 plus n_anchor * (vocab/64) * 8
+ *   must fit in the array (at most 126 anchors at vocab 128256, 508 at 32000);
  *   larger requests return ALR_E_WORKSPACE before anything is enqueued.
  * Every entry of the scratch a call reads is first written by that call, so
  * nothing needs clearing between calls.  All calls on one device share the one

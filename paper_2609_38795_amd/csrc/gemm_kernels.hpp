@@ -248,27 +248,24 @@ struct EpiSwiGLU {
 };
 
 // Per-row statistics of the output-head logits over one 64-column group: the
-// group's max m, s = sum of exp(z - m) over its 64 entries, and the lowest
-// column holding the max.  The finalisation merges a row's groups into its
-// log-sum-exp and argmax without another pass over the logits.
+// group's max m and s = sum of exp(z - m) over its 64 entries.  The
+// finalisation merges a row's groups into its log-sum-exp without another pass
+// over the logits (and finds the lowest column holding the max in its one pass).
 struct LogitPart {
   float m, s;
-  int i;
 };
 
 // LogitPart of one row over the 64-column group held by a 32-lane half-wave:
-// lane lr of the half holds column c = 64 g + lr (lo) and c + 32 (hi).  Every
+// lane lr of the half holds column 64 g + lr (lo) and that + 32 (hi).  Every
 // lane of the half must call this with the same row; the result is the same
 // in all of them.
-__device__ __forceinline__ LogitPart half_wave_part(float lo, float hi, int c) {
+__device__ __forceinline__ LogitPart half_wave_part(float lo, float hi) {
   float mx = group_max<16>(fmaxf(lo, hi));
   mx = max_xor16(mx);
-  int arg = (lo == mx) ? c : ((hi == mx) ? c + 32 : 0x7FFFFFFF);
-  arg = min_xor16_i(group_min16_i(arg));
   const float l2e = 1.44269504088896341f;
   float e = fast_exp2((lo - mx) * l2e) + fast_exp2((hi - mx) * l2e);
   e = sum_xor16(group_sum<16>(e));
-  return {mx, e, arg};
+  return {mx, e};
 }
 
 // fp32 logits into caller rows: out + (perm ? perm[row] : row) * rs; with part,
@@ -288,7 +285,7 @@ struct EpiLogits {
     p[0] = lo;
     p[32] = hi;
     if (part) {
-      const LogitPart q = half_wave_part(lo, hi, c);
+      const LogitPart q = half_wave_part(lo, hi);
       if ((threadIdx.x & 31) == 0) part[(long)row * part_ld + (c >> 6)] = q;
     }
   }
@@ -310,10 +307,10 @@ struct EpiLogits {
     if (part) {
       // all 16 rows reduced over the half-wave; lane lr < 16 then stores row t = lr
       const int lr = threadIdx.x & 31;
-      LogitPart mine = {0.f, 0.f, 0};
+      LogitPart mine = {0.f, 0.f};
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        const LogitPart q = half_wave_part(lo[t], hi[t], c);
+        const LogitPart q = half_wave_part(lo[t], hi[t]);
         if (lr == t) mine = q;
       }
       const int r = rb + 8 * (lr >> 2) + (lr & 3);

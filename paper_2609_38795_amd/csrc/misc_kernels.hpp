@@ -141,11 +141,12 @@ __global__ __launch_bounds__(256) void scatter_rows_kernel(char* __restrict__ ds
 // Output head finalisation of the sorted row r of slot s.
 //   Logits (fp32, V entries) of row r are at z + (z_perm ? perm[r] : r) * z_rs,
 //   written by the output-head GEMM.  Outputs go to index o = perm[r] * block + s
-//   (the caller's anchor order).  The row's max, argmax (ties -> lowest id) and
-//   sum(exp(z - max)) come from the GEMM epilogue's per-group partials
-//   (part[r * part_ld + g], g < part_ld = V / 64) when part is set, else from a
-//   first pass over the logits.  Then one pass (when write_lp or TOPK) rewrites
-//   the row as z - LSE and, with TOPK, keeps each thread's 8 best (value, id)
+//   (the caller's anchor order).  The row's max and sum(exp(z - max)) come from
+//   the GEMM epilogue's per-group partials (part[r * part_ld + g], g < part_ld =
+//   V / 64) when part is set, and the argmax (ties -> lowest id) is then the
+//   first column equal to the max, found in the pass below; without partials a
+//   first pass over the logits gives all three.  Then one pass rewrites the row
+//   as z - LSE (write_lp) and, with TOPK, keeps each thread's 8 best (value, id)
 //   pairs, ranked by decreasing value and then increasing id, while summing
 //   exp(z - max) over every entry the thread drops from (or never admits to)
 //   that list; eight block-wide argmax rounds merge the lists into the row's
@@ -224,11 +225,12 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
     return;
   }
   MaxArg acc = {-INFINITY, 0.f, 0x7FFFFFFF};
-  if (a.part != nullptr) {
+  const bool from_part = a.part != nullptr;
+  if (from_part) {
     const LogitPart* pr = a.part + (long)r * a.part_ld;
     for (int g = threadIdx.x; g < a.part_ld; g += blockDim.x) {
       const LogitPart q = pr[g];
-      acc = merge_maxarg(acc, MaxArg{q.m, q.s, q.i});
+      acc = merge_maxarg(acc, MaxArg{q.m, q.s, 0x7FFFFFFF});
     }
   } else {
     for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
@@ -255,21 +257,25 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   }
   if (lane == 0) red[wave] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    MaxArg t = red[0];
-    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) t = merge_maxarg(t, red[w]);
-    lse_sh = t.m + logf(t.s);
-    m_sh = t.m;
-    s_sh = t.s;
-    if (a.tokens) a.tokens[o] = t.i;
+  // the greedy token (or the forced one) goes out once the argmax is known
+  auto emit_token = [&](int arg) {
+    if (a.tokens) a.tokens[o] = arg;
     if (a.next_tok) {
-      int nxt = t.i;
+      int nxt = arg;
       if (a.forced != nullptr) {
         const int f = a.forced[o];
         if (f >= 0) nxt = f;
       }
       a.next_tok[r] = nxt;
     }
+  };
+  if (threadIdx.x == 0) {
+    MaxArg t = red[0];
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) t = merge_maxarg(t, red[w]);
+    lse_sh = t.m + logf(t.s);
+    m_sh = t.m;
+    s_sh = t.s;
+    if (!from_part) emit_token(t.i);
     if (a.target) {
       const int x = a.target[r];
       tgt_sh = (x >= 0) ? z[x] : __builtin_nanf("");
@@ -277,7 +283,7 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   }
   __syncthreads();
   const float lse = lse_sh, m = m_sh;
-  if (!a.write_lp && !TOPK) {
+  if (!a.write_lp && !TOPK && !from_part) {
     if (a.target && threadIdx.x == 0) a.target_logp[o] = tgt_sh - lse;
     return;
   }
@@ -289,10 +295,12 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
     ti[j] = 0x7FFFFFFF;
   }
   float tsum = 0.f;  // exp(z - m) of the entries this thread dropped or never admitted
+  int arg = 0x7FFFFFFF;  // this thread's first column equal to the row max
   for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
     f32x4 v = *(const f32x4*)(z + c);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
+      if (arg == 0x7FFFFFFF && v[e] == m) arg = c + e;  // columns rise within a thread
       if constexpr (TOPK) {
         // this thread meets ids in increasing order, so an equal value ranks
         // after the entries already held: admit only strictly larger values
@@ -322,6 +330,18 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
       v[e] -= lse;
     }
     if (a.write_lp) *(f32x4*)(z + c) = v;
+  }
+  if (from_part) {  // lowest column holding the max over the block
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) arg = min(arg, __shfl_xor(arg, off));
+    if (lane == 0) win_i[wave] = arg;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int t = win_i[0];
+      for (int w = 1; w < (int)(blockDim.x >> 6); ++w) t = min(t, win_i[w]);
+      emit_token(t);
+    }
+    __syncthreads();  // win_i is reused by the top-8 rounds
   }
   if constexpr (TOPK) {
     // eight rounds: the best head of all threads' lists is the next entry

@@ -60,8 +60,11 @@ def test_noalloc_equals_workspace_rollout_topk(dtype):
         print(f"  {n} anchors: tokens, top-8 ids and log-probs, tails and features bit-identical",
               flush=True)
     # a request whose logit rows would not fit the fixed array is refused up front
-    per_row = V * 4 + (V // 64) * 12
-    n_big = (64 << 20) // per_row + 1
+    # the documented limit: 256-aligned n * V * 4 plus n * (V / 64) * 8 bytes within 64 MiB
+    fits = lambda n: ((n * V * 4 + 255) // 256) * 256 + n * (V // 64) * 8 <= (64 << 20)
+    n_big = 1
+    while fits(n_big):
+        n_big += 1
     big = np.arange(n_big) % w.n_anchors
     with pytest.raises(binding.AlrError) as ei:
         eng.rollout_topk_noalloc(inp.anchor_seq[big], inp.anchor_pos[big], B, out)
