@@ -222,12 +222,13 @@ def embed_rows(P: Params, tokens: Sequence[int], given_rows: Optional[np.ndarray
 
 def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
                     emulate_bf16: bool = False, want_layers: bool = True,
-                    bf16_probs: bool = False):
+                    bf16_probs: bool = False, progress=None):
     """Full causal forward.  Returns (outputs of every layer [L][T,d], final-normed [T,d]).
 
     bf16_probs: with emulate_bf16, attention also rounds its unnormalised
     probabilities to bf16 before the value product (a second valid bf16
-    evaluation, used to size the bf16 noise floor)."""
+    evaluation, used to size the bf16 noise floor).  progress(layer) (optional) is
+    called after each layer (long evaluations report as they go)."""
     rnd = bf16_round if emulate_bf16 else _ident
     rp = bf16_round if (emulate_bf16 and bf16_probs) else None
     dt = P.dt
@@ -251,6 +252,8 @@ def decoder_forward(P: Params, shape, x0: np.ndarray, positions: np.ndarray,
         h = h + act @ P.get("w_down", layer).T
         if want_layers:
             outs.append(h.copy())
+        if progress is not None:
+            progress(layer)
     hf = rnd(rmsnorm(h, P.get("final_norm"), eps))
     return outs, hf
 
@@ -385,13 +388,13 @@ def rollout_naive(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos, 
 def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anchor_pos,
                            block: int, feed: np.ndarray, given_rows=None, given_mask=None,
                            emulate_bf16: bool = False, want_logprobs: bool = True,
-                           positions=None, bf16_probs: bool = False):
+                           positions=None, bf16_probs: bool = False, progress=None):
     """One causal forward per anchor over x_{<=a} . feed[i, :B-1], read at positions a..a+B-1.
 
     feed[n, B] holds the token fed *after* each slot (column B-1 is unused), i.e.
     the input of slot s+1 is feed[i, s].  Returns (argmax tokens [n,B],
     logprobs [n,B,V] or None, feats [n,B,n_feat,d], top-2 margins [n,B]).
-    bf16_probs: see :func:`decoder_forward`.
+    bf16_probs, progress: see :func:`decoder_forward`.
     """
     n = len(anchor_seq)
     V, d, nf = shape.vocab, shape.d_model, len(shape.feat_layers)
@@ -408,7 +411,7 @@ def rollout_teacher_forced(P: Params, shape, tokens: np.ndarray, anchor_seq, anc
         rows = np.concatenate([prefix, embed_rows(P, fed)], 0) if fed else prefix
         pos_seq = None if positions is None else positions[sq]
         outs, hf = decoder_forward(P, shape, rows, slot_positions(pos_seq, a, len(fed)),
-                                   emulate_bf16, bf16_probs=bf16_probs)
+                                   emulate_bf16, bf16_probs=bf16_probs, progress=progress)
         z = head_logits(P, hf[a:a + block])
         lp = log_softmax(z)
         if want_logprobs:

@@ -28,6 +28,7 @@ attention rounds).
 from __future__ import annotations
 
 import dataclasses
+import time
 from typing import Optional
 
 import numpy as np
@@ -72,14 +73,29 @@ def _given(inp, sel_seq):
     return rows, mask
 
 
+def _layer_progress(shape, what):
+    """Per-layer progress lines for evaluations of deep, wide models (minutes each)."""
+    if shape.n_params() < 1_000_000_000:
+        return None
+    t0 = time.time()
+
+    def report(layer):
+        if (layer + 1) % 8 == 0 or layer + 1 == shape.n_layers:
+            print(f"[oracle] {what}: layer {layer + 1}/{shape.n_layers} "
+                  f"({time.time() - t0:.0f}s)", flush=True)
+    return report
+
+
 def oracle_rollout(inp, shape, anchor_seq, anchor_pos, block, feed, emulate, dt=np.float64,
                    positions=None, bf16_probs=False):
     """Teacher-forced oracle along ``feed`` (tokens fed after each slot)."""
     P = O.Params(inp.weights, dt=dt, cache=shape.n_params() < 400_000_000)
     rows, mask = _given(inp, anchor_seq)
+    what = f"{np.dtype(dt).name}{' bf16-probs' if bf16_probs else ''} anchors {list(anchor_pos)}"
     return O.rollout_teacher_forced(P, shape, inp.tokens, anchor_seq, anchor_pos, block, feed,
                                     given_rows=rows, given_mask=mask, emulate_bf16=emulate,
-                                    positions=positions, bf16_probs=bf16_probs)
+                                    positions=positions, bf16_probs=bf16_probs,
+                                    progress=_layer_progress(shape, what))
 
 
 def compare(inp, shape, sel, gpu_run, block, measure_floor: Optional[bool] = None,
