@@ -28,10 +28,12 @@ extern "C" {
  * summed in slice order by a second kernel; 2 or 4 slices by the library's
  * rule, at least 2; K a multiple of 128); 19 = the ping-pong kernel of 17 run
  * persistently (one workgroup per CU looping over the tiles, the next tile's
- * first k-steps loaded during the current tile's last ones).  Other values:
- * ALR_E_INVALID_ARG.  Tile 18 needs a device scratch buffer of at least
- * 2*M*N*4 bytes for the partial sums (up to 4*M*N*4 are used when given);
- * ALR_E_WORKSPACE otherwise.
+ * first k-steps loaded during the current tile's last ones); 20 = split-K
+ * over the 64x128 kernel of 3 (2 or 4 slices, each a multiple of 64; the
+ * unsplit kernel of 3 when K allows no split).  Other values:
+ * ALR_E_INVALID_ARG.  Tiles 18 and 20 need a device scratch buffer of at
+ * least 2*M*N*4 bytes for the partial sums (up to 4*M*N*4 are used when
+ * given); ALR_E_WORKSPACE otherwise.
  * Enqueued on `stream`. */
 alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C, int32_t M,
                           int32_t N, int32_t K, int32_t tile, void* scratch,

@@ -26,7 +26,8 @@ EXPORTS = ("alr_workspace_bytes", "alr_check_config", "alr_check_rollout", "alr_
            "alr_prefill", "alr_prefill_positions", "alr_rollout", "alr_rollout_topk",
            "alr_rollout_topk_noalloc",
            "alr_corpus_labels", "alr_ira_assemble", "alr_slot_weights", "alr_last_error", "alr_status_string", "alr_destroy",
-           "alr_debug_gemm", "alr_debug_decode_plan", "alr_profile_start", "alr_profile_stop")
+           "alr_debug_gemm", "alr_debug_decode_plan", "alr_profile_start", "alr_profile_stop",
+           "alr_set_rollout_graphs")
 ALR_TOPK = 8
 
 
@@ -120,6 +121,8 @@ def load_library() -> ctypes.CDLL:
     lib.alr_profile_start.restype = ctypes.c_int
     lib.alr_profile_stop.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
     lib.alr_profile_stop.restype = ctypes.c_int
+    lib.alr_set_rollout_graphs.argtypes = [vp, i32]
+    lib.alr_set_rollout_graphs.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -248,6 +251,12 @@ class Engine:
 
     def _err(self, st: int):
         raise AlrError(st, self.lib.alr_last_error(self.ctx).decode())
+
+    def set_rollout_graphs(self, enable: bool):
+        """alr_set_rollout_graphs: replay recorded launch graphs for repeated rollouts."""
+        st = self.lib.alr_set_rollout_graphs(self.ctx, 1 if enable else 0)
+        if st != 0:
+            self._err(st)
 
     def close(self):
         if getattr(self, "ctx", None):
@@ -439,7 +448,7 @@ def debug_gemm(dtype: int, A, W, C, stream=None, tile: int = 0):
     N = W.shape[0]
     scratch = None
     nbytes = 0
-    if dtype == ALR_BF16 and tile == 18:
+    if dtype == ALR_BF16 and tile in (18, 20):
         nbytes = 4 * M * N * 4
         scratch = torch.empty(nbytes, dtype=torch.uint8, device=A.device)
     st = lib.alr_debug_gemm(dtype, A.data_ptr(), W.data_ptr(), C.data_ptr(), M, N, K, tile,

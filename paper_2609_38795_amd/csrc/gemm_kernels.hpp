@@ -524,11 +524,12 @@ __device__ __forceinline__ void gemm_stage_mma(const bf16* As, const bf16* Ws, i
 
 // TAG only separates the instantiations of different call sites, so that
 // profilers report each GEMM of the model on its own line.  K must be a
-// multiple of 2*BK.
+// multiple of 2*BK.  With splits > 1 (an epilogue with set_split) workgroup b
+// computes K slice b % splits of tile b / splits, K being the slice length.
 template <int TAG, int BM, int BN, int WGM, int WGN, int BK, int OCC, class Epi>
 __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
     const bf16* __restrict__ A, int lda, const bf16* __restrict__ W, int ldw, int M, int N, int K,
-    int tiles_m, int tiles_n, Epi epi) {
+    int tiles_m, int tiles_n, Epi epi, int splits = 1) {
   constexpr int NT = 64 * WGM * WGN;  // threads
   constexpr int WTM = BM / WGM;  // wave tile rows
   constexpr int WTN = BN / WGN;  // wave tile columns (multiple of 64: epilogue pairs c, c+32)
@@ -542,8 +543,18 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM * BK];
   __shared__ __attribute__((aligned(16))) bf16 Ws[2][BN * BK];
 
+  int bid = blockIdx.x;
+  if constexpr (has_set_split<Epi>::value) {
+    if (splits > 1) {
+      const int sl = bid % splits;
+      bid /= splits;
+      A += (long)sl * K;
+      W += (long)sl * K;
+      epi.set_split(sl);
+    }
+  }
   int tm, tn;
-  gemm_tile_coords(tiles_m, tiles_n, tm, tn);
+  gemm_tile_coords(bid, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;

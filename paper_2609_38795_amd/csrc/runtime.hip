@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -327,6 +328,17 @@ struct alr_ctx {
   int prof_site = 0;
   std::vector<hipEvent_t> prof_ev;
   size_t prof_used = 0;
+  // rollout launch graphs (alr_set_rollout_graphs): the instantiated graphs,
+  // least recently used first, and the private stream they are recorded and
+  // replayed on, ordered after and before the caller's stream by two events
+  struct RolloutGraph {
+    std::array<uintptr_t, 12> key;
+    hipGraphExec_t exec;
+  };
+  bool graphs_on = true;
+  std::vector<RolloutGraph> graphs;
+  hipStream_t graph_stream = nullptr;
+  hipEvent_t graph_in = nullptr, graph_out = nullptr;
 
   template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(ws + off); }
   char* layer(int l) const { return ws + L.layer0 + (size_t)l * L.layer_stride; }
@@ -427,6 +439,36 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     // tile; a split-K reduce hands it columns in another arrangement
     bool epi_whole_k = false;
     if constexpr (std::is_same<Epi, EpiLogits>::value) epi_whole_k = epi.part != nullptr;
+    // Few rows (the rollout of a small batch): when even split-K leaves more
+    // than half the CUs without a 256x256 tile, 64x128 tiles split over K
+    // (slices of >= 256 and a multiple of 64) spread the work over more CUs.
+    if ((cfg == 20 || (cfg == 0 && !fill128)) && ctx->splitk_buf != nullptr && !epi_whole_k) {
+      const int t256 = tiles(256, 256), t64 = tiles(64, 128);
+      int S256 = 1, S = 1;
+      for (int cand : {2, 4}) {
+        const bool fits = (size_t)cand * M * N * 4 <= ctx->splitk_bytes;
+        if ((long)t256 * cand <= ctx->n_cu && K % (64 * cand) == 0 && K / cand >= 512 && fits)
+          S256 = cand;
+        if ((long)t64 * cand <= ctx->n_cu && K % (64 * cand) == 0 &&
+            (K / cand >= 256 || cfg == 20) && fits)
+          S = cand;
+      }
+      if (S > 1 && (cfg == 20 || ((long)t256 * S256 < ctx->n_cu / 2 && t64 * S >= 2 * t256 * S256))) {
+        const int tm = (M + 63) / 64, tn = (N + 127) / 128;
+        EpiPartial ep{ctx->splitk_buf, (long)M * N, N};
+        if ((K / S) % 128 == 0)
+          gemm_bf16_kernel<TAG, 64, 128, 2, 2, 64, 2, EpiPartial>
+              <<<t64 * S, 256, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
+        else
+          gemm_bf16_kernel<TAG, 64, 128, 2, 2, 32, 4, EpiPartial>
+              <<<t64 * S, 256, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
+        const long thr = (long)M * (N / 64) * 32;
+        splitk_reduce_kernel<Epi>
+            <<<(unsigned)((thr + 255) / 256), 256, 0, st>>>(ctx->splitk_buf, (long)M * N, S, M, N, epi);
+        return;
+      }
+      if (cfg == 20) cfg = 3;
+    }
     if ((cfg == 18 || (cfg == 0 && !fill128)) && ctx->splitk_buf != nullptr && !epi_whole_k) {
       const int t256 = tiles(256, 256);
       int S = 1;
@@ -799,6 +841,83 @@ alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, c
     stt = lm_head<T>(ctx, n, s, block, forced, out, true, nullptr, st);
     if (stt != ALR_OK) return stt;
   }
+  return ALR_OK;
+}
+
+constexpr size_t kMaxRolloutGraphs = 4;
+
+void drop_rollout_graphs(alr_ctx* ctx) {
+  for (auto& g : ctx->graphs) (void)hipGraphExecDestroy(g.exec);
+  ctx->graphs.clear();
+}
+
+// rollout_impl through a cached HIP graph.  Besides the context's constants,
+// the launches of one rollout depend only on the key below (anchor count,
+// block, the size of the attention work list, the output and input pointers):
+// anchors, positions and plans reach the kernels through the workspace and are
+// uploaded on the caller's stream before the graph runs, so a graph recorded
+// for one call replays every later call with the same key.  The graph is
+// recorded and run on the context's own stream (the null stream cannot be
+// captured), which waits for the caller's stream and which the caller's stream
+// then waits for.  Plain launches while a launch site of the rollout is being
+// timed (its event pairs are recorded per launch), when the caller's stream is
+// itself being captured, or when graphs are off.
+template <typename T>
+alr_status run_rollout(alr_ctx* ctx, int n, int block, const int32_t* forced, const LabelDst& out,
+                       float* feats_out, hipStream_t st, bool allow_graph) {
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  const bool timing_rollout_site = ctx->prof_site >= ALR_PROF_DECODE_QKV;
+  if (!allow_graph || !ctx->graphs_on || timing_rollout_site || n <= 0)
+    return rollout_impl<T>(ctx, n, block, forced, out, feats_out, st);
+  ALR_HIP(ctx, hipStreamIsCapturing(st, &cap));
+  if (cap != hipStreamCaptureStatusNone)
+    return rollout_impl<T>(ctx, n, block, forced, out, feats_out, st);
+  if (!ctx->graph_stream) {
+    ALR_HIP(ctx, hipStreamCreateWithFlags(&ctx->graph_stream, hipStreamNonBlocking));
+    ALR_HIP(ctx, hipEventCreateWithFlags(&ctx->graph_in, hipEventDisableTiming));
+    ALR_HIP(ctx, hipEventCreateWithFlags(&ctx->graph_out, hipEventDisableTiming));
+  }
+  hipStream_t gs = ctx->graph_stream;
+  const std::array<uintptr_t, 12> key{
+      (uintptr_t)n, (uintptr_t)block, (uintptr_t)ctx->h_dwork.size(), (uintptr_t)forced,
+      (uintptr_t)feats_out, (uintptr_t)out.logprobs, (uintptr_t)out.tokens,
+      (uintptr_t)out.top_ids, (uintptr_t)out.top_logp, (uintptr_t)out.tail,
+      (uintptr_t)out.logit_rows, (uintptr_t)out.part_rows};
+  ALR_HIP(ctx, hipEventRecord(ctx->graph_in, st));
+  ALR_HIP(ctx, hipStreamWaitEvent(gs, ctx->graph_in, 0));
+  hipGraphExec_t exec = nullptr;
+  for (size_t i = 0; i < ctx->graphs.size(); ++i) {
+    if (ctx->graphs[i].key == key) {
+      const alr_ctx::RolloutGraph g = ctx->graphs[i];
+      ctx->graphs.erase(ctx->graphs.begin() + (long)i);
+      ctx->graphs.push_back(g);
+      exec = g.exec;
+      break;
+    }
+  }
+  if (!exec) {
+    ALR_HIP(ctx, hipStreamBeginCapture(gs, hipStreamCaptureModeThreadLocal));
+    const alr_status rs = rollout_impl<T>(ctx, n, block, forced, out, feats_out, gs);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(gs, &graph);
+    if (rs != ALR_OK || ec != hipSuccess || !graph) {
+      if (graph) (void)hipGraphDestroy(graph);
+      if (rs != ALR_OK) return rs;
+      return fail(ctx, ALR_E_HIP, "rollout graph capture failed: %s", hipGetErrorString(ec));
+    }
+    const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ei != hipSuccess)
+      return fail(ctx, ALR_E_HIP, "rollout graph instantiation failed: %s", hipGetErrorString(ei));
+    if (ctx->graphs.size() >= kMaxRolloutGraphs) {
+      (void)hipGraphExecDestroy(ctx->graphs.front().exec);
+      ctx->graphs.erase(ctx->graphs.begin());
+    }
+    ctx->graphs.push_back({key, exec});
+  }
+  ALR_HIP(ctx, hipGraphLaunch(exec, gs));
+  ALR_HIP(ctx, hipEventRecord(ctx->graph_out, gs));
+  ALR_HIP(ctx, hipStreamWaitEvent(st, ctx->graph_out, 0));
   return ALR_OK;
 }
 
@@ -1361,8 +1480,8 @@ alr_status alr_rollout(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq
   if (st != ALR_OK) return st;
   const LabelDst out{logprobs_out, tokens_out, nullptr, nullptr, nullptr};
   return (ctx->cfg.dtype == ALR_BF16)
-             ? rollout_impl<bf16>(ctx, n_anchor, block, forced, out, feats_out, s)
-             : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
+             ? run_rollout<bf16>(ctx, n_anchor, block, forced, out, feats_out, s, true)
+             : run_rollout<float>(ctx, n_anchor, block, forced, out, feats_out, s, true);
 }
 
 alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
@@ -1379,8 +1498,8 @@ alr_status alr_rollout_topk(alr_ctx* ctx, int32_t n_anchor, const int32_t* ancho
   if (st != ALR_OK) return st;
   const LabelDst out{logprobs_out, tokens_out, top_ids_out, top_logp_out, tail_out};
   return (ctx->cfg.dtype == ALR_BF16)
-             ? rollout_impl<bf16>(ctx, n_anchor, block, forced, out, feats_out, s)
-             : rollout_impl<float>(ctx, n_anchor, block, forced, out, feats_out, s);
+             ? run_rollout<bf16>(ctx, n_anchor, block, forced, out, feats_out, s, true)
+             : run_rollout<float>(ctx, n_anchor, block, forced, out, feats_out, s, true);
 }
 
 alr_status alr_rollout_topk_noalloc(alr_ctx* ctx, int32_t n_anchor, const int32_t* anchor_seq,
@@ -1504,9 +1623,23 @@ const char* alr_last_error(const alr_ctx* ctx) {
   return ctx ? ctx->err.c_str() : g_create_err.c_str();
 }
 
+alr_status alr_set_rollout_graphs(alr_ctx* ctx, int32_t enable) {
+  if (!ctx) return ALR_E_INVALID_ARG;
+  if (enable != 0 && enable != 1)
+    return fail(ctx, ALR_E_INVALID_ARG, "enable must be 0 or 1, got %d", enable);
+  ctx->graphs_on = enable == 1;
+  if (!ctx->graphs_on) drop_rollout_graphs(ctx);
+  return ALR_OK;
+}
+
 void alr_destroy(alr_ctx* ctx) {
   if (!ctx) return;
   for (hipEvent_t e : ctx->prof_ev) (void)hipEventDestroy(e);
+  if (ctx->graph_stream) (void)hipStreamSynchronize(ctx->graph_stream);
+  drop_rollout_graphs(ctx);
+  if (ctx->graph_in) (void)hipEventDestroy(ctx->graph_in);
+  if (ctx->graph_out) (void)hipEventDestroy(ctx->graph_out);
+  if (ctx->graph_stream) (void)hipStreamDestroy(ctx->graph_stream);
   delete ctx;
 }
 
@@ -1574,7 +1707,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
                           size_t scratch_bytes, alr_stream stream) {
   if (!A || !W || !C || M <= 0 || N <= 0 || K <= 0) return ALR_E_INVALID_ARG;
   if (N % 64 || K % 64) return ALR_E_UNSUPPORTED;
-  if (tile < 0 || (tile > 5 && tile < 17) || tile > 19) return ALR_E_INVALID_ARG;
+  if (tile < 0 || (tile > 5 && tile < 17) || tile > 20) return ALR_E_INVALID_ARG;
   hipStream_t s = static_cast<hipStream_t>(stream);
   EpiLogits el;
   el.out = C;
@@ -1585,7 +1718,7 @@ alr_status alr_debug_gemm(int32_t dtype, const void* A, const void* W, float* C,
   alr_ctx dummy;
   if (dtype == ALR_BF16) {
     const bf16* Wk = (const bf16*)W;
-    if (tile == 18) {  // split-K: partial sums in the scratch buffer
+    if (tile == 18 || tile == 20) {  // split-K: partial sums in the scratch buffer
       if (!splitk_scratch || scratch_bytes < (size_t)2 * M * N * 4) return ALR_E_WORKSPACE;
       dummy.splitk_buf = static_cast<float*>(splitk_scratch);
       dummy.splitk_bytes = scratch_bytes;

@@ -21,8 +21,9 @@ def _print(*a):
 # ------------------------------------------------------------------ GEMM kernels
 @pytest.mark.parametrize("dtype,tile", [("bf16", 0), ("f32", 0), ("bf16", 1), ("bf16", 2),
                                         ("bf16", 3), ("bf16", 4), ("bf16", 5), ("bf16", 17),
-                                        ("bf16", 18), ("bf16", 19)])
-@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 192, 256), (1024, 640, 1152)])
+                                        ("bf16", 18), ("bf16", 19), ("bf16", 20)])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 192, 256), (1024, 640, 1152),
+                                   (257, 320, 1536)])
 def test_gemm_kernel(dtype, tile, M, N, K):
     """Every GEMM kernel variant against a float64 product, ragged M and partial N tiles."""
     _print(f"gemm {dtype} tile {tile} {M}x{N}x{K}")
