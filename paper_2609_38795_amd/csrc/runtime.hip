@@ -846,7 +846,11 @@ alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, c
 
 constexpr size_t kMaxRolloutGraphs = 4;
 
+// The graphs run on the context's own stream: waiting for it first means no
+// graph is destroyed while a launch of it may still execute.
 void drop_rollout_graphs(alr_ctx* ctx) {
+  if (ctx->graphs.empty()) return;
+  (void)hipStreamSynchronize(ctx->graph_stream);
   for (auto& g : ctx->graphs) (void)hipGraphExecDestroy(g.exec);
   ctx->graphs.clear();
 }
@@ -872,10 +876,21 @@ alr_status run_rollout(alr_ctx* ctx, int n, int block, const int32_t* forced, co
   ALR_HIP(ctx, hipStreamIsCapturing(st, &cap));
   if (cap != hipStreamCaptureStatusNone)
     return rollout_impl<T>(ctx, n, block, forced, out, feats_out, st);
-  if (!ctx->graph_stream) {
-    ALR_HIP(ctx, hipStreamCreateWithFlags(&ctx->graph_stream, hipStreamNonBlocking));
-    ALR_HIP(ctx, hipEventCreateWithFlags(&ctx->graph_in, hipEventDisableTiming));
-    ALR_HIP(ctx, hipEventCreateWithFlags(&ctx->graph_out, hipEventDisableTiming));
+  if (!ctx->graph_stream) {  // all three or none
+    hipStream_t gs0 = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&gs0, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&e0, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&e1, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      if (e1) (void)hipEventDestroy(e1);
+      if (e0) (void)hipEventDestroy(e0);
+      if (gs0) (void)hipStreamDestroy(gs0);
+      return fail(ctx, ALR_E_HIP, "rollout graph stream or events: %s", hipGetErrorString(e));
+    }
+    ctx->graph_stream = gs0;
+    ctx->graph_in = e0;
+    ctx->graph_out = e1;
   }
   hipStream_t gs = ctx->graph_stream;
   const std::array<uintptr_t, 12> key{
@@ -910,6 +925,8 @@ alr_status run_rollout(alr_ctx* ctx, int n, int block, const int32_t* forced, co
     if (ei != hipSuccess)
       return fail(ctx, ALR_E_HIP, "rollout graph instantiation failed: %s", hipGetErrorString(ei));
     if (ctx->graphs.size() >= kMaxRolloutGraphs) {
+      // the least recently used graph may be the last one launched on gs
+      ALR_HIP(ctx, hipStreamSynchronize(gs));
       (void)hipGraphExecDestroy(ctx->graphs.front().exec);
       ctx->graphs.erase(ctx->graphs.begin());
     }
@@ -1635,7 +1652,6 @@ alr_status alr_set_rollout_graphs(alr_ctx* ctx, int32_t enable) {
 void alr_destroy(alr_ctx* ctx) {
   if (!ctx) return;
   for (hipEvent_t e : ctx->prof_ev) (void)hipEventDestroy(e);
-  if (ctx->graph_stream) (void)hipStreamSynchronize(ctx->graph_stream);
   drop_rollout_graphs(ctx);
   if (ctx->graph_in) (void)hipEventDestroy(ctx->graph_in);
   if (ctx->graph_out) (void)hipEventDestroy(ctx->graph_out);

@@ -118,3 +118,26 @@ def test_set_rollout_graphs_rejects_other_values():
     st = eng.lib.alr_set_rollout_graphs(eng.ctx, 2)
     assert st != 0
     eng.close()
+
+
+def test_rollout_graph_cache_eviction():
+    """Five keys (five output tensor sets) cycled twice through the four-entry graph cache: every call
+    after an eviction records again, and every result equals plain launches."""
+    inp = _workload()
+    w = inp.workload
+    n = len(inp.anchor_seq)
+    eng = make_engine(inp, max_anchors=n, max_block=w.block)
+    prefill(eng, inp)
+    eng.set_rollout_graphs(False)
+    ref = _host(eng.rollout(inp.anchor_seq, inp.anchor_pos, w.block))
+    eng.set_rollout_graphs(True)
+    outs = [eng.alloc_outputs(n, w.block, True) for _ in range(5)]
+    for rnd in range(2):
+        for i, o in enumerate(outs):
+            _print(f"  round {rnd}, output set {i}")
+            got = _host(eng.rollout(inp.anchor_seq, inp.anchor_pos, w.block, out=o))
+            _same(got, ref, f"round {rnd}, output set {i}")
+    # switching graphs off drops the cache; plain launches still match
+    eng.set_rollout_graphs(False)
+    _same(_host(eng.rollout(inp.anchor_seq, inp.anchor_pos, w.block, out=outs[0])), ref, "graphs off")
+    eng.close()
