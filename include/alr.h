@@ -256,24 +256,29 @@ alr_status alr_rollout_topk_noalloc(alr_ctx* ctx, int32_t n_anchor, const int32_
                                     float* feats_out, alr_stream stream);
 
 /* Rollout launch graphs.  A launch mechanism, not an operation of the method:
- * results are bit-identical with graphs on or off.  When on (the default),
- * alr_rollout and alr_rollout_topk record their kernel launches (one per layer
- * step, thousands per call) into a HIP graph the first time a combination of
- * n_anchor, block, the size of the decode attention work list, `forced`,
- * `feats_out` and every output pointer is seen, and replay that graph for later
- * calls with the same combination.  Anchors, positions and attention plans are
- * uploaded by every call before its graph runs, so the anchors themselves may
- * differ between replays, and a new prefill leaves the graphs valid.  The graphs
- * run on a stream of the context's own that first waits for the work already
- * on the caller's `stream`; later work on `stream` waits for the graph.  Up to
- * 4 graphs are kept per context (the least recently used is dropped); the first
- * call of a combination costs the recording and instantiation on the host.
+ * results are bit-identical with graphs on or off.  Off by default (then
+ * nothing is allocated after alr_create).  When turned on, alr_rollout and
+ * alr_rollout_topk record their kernel launches (one per layer step, thousands
+ * per call) into a HIP graph the first time a combination of n_anchor, block,
+ * the size of the decode attention work list, `forced`, `feats_out` and every
+ * output pointer is seen, and replay that graph for later calls with the same
+ * combination.  Anchors, positions and attention plans are uploaded by every
+ * call before its graph runs, so the anchors themselves may differ between
+ * replays, and a new prefill leaves the graphs valid.  The graphs run on a
+ * stream of the context's own that first waits for the work already on the
+ * caller's `stream`; later work on `stream` waits for the graph.  Up to 4
+ * graphs are kept per context (the least recently used is dropped, after the
+ * context's stream has drained); the first call of a combination costs the
+ * recording and instantiation on the host.
  * Not used by alr_rollout_topk_noalloc (instantiation allocates), while a
  * launch site of the rollout is being timed (alr_profile_start with a rollout
  * or output-head site), or when `stream` is itself being captured (the
  * launches then go into the caller's own graph).
- *   enable: 1 on, 0 off (also drops the cached graphs).
- * Errors: ALR_E_INVALID_ARG for a NULL ctx or another value of enable. */
+ *   enable: 1 on (the first time, creates the context's stream and two events;
+ *           each recorded graph holds the runtime's resources for its
+ *           instantiation until it is dropped), 0 off (drops the cached graphs).
+ * Errors: ALR_E_INVALID_ARG for a NULL ctx or another value of enable; ALR_E_HIP
+ * if the stream or events cannot be created (graphs stay off). */
 alr_status alr_set_rollout_graphs(alr_ctx* ctx, int32_t enable);
 
 /* Fixed-corpus distillation labels and erase gates (Sec. 3.1: the KD labels

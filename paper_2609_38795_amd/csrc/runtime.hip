@@ -335,7 +335,7 @@ struct alr_ctx {
     std::array<uintptr_t, 12> key;
     hipGraphExec_t exec;
   };
-  bool graphs_on = true;
+  bool graphs_on = false;
   std::vector<RolloutGraph> graphs;
   hipStream_t graph_stream = nullptr;
   hipEvent_t graph_in = nullptr, graph_out = nullptr;
@@ -876,23 +876,7 @@ alr_status run_rollout(alr_ctx* ctx, int n, int block, const int32_t* forced, co
   ALR_HIP(ctx, hipStreamIsCapturing(st, &cap));
   if (cap != hipStreamCaptureStatusNone)
     return rollout_impl<T>(ctx, n, block, forced, out, feats_out, st);
-  if (!ctx->graph_stream) {  // all three or none
-    hipStream_t gs0 = nullptr;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    hipError_t e = hipStreamCreateWithFlags(&gs0, hipStreamNonBlocking);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&e0, hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&e1, hipEventDisableTiming);
-    if (e != hipSuccess) {
-      if (e1) (void)hipEventDestroy(e1);
-      if (e0) (void)hipEventDestroy(e0);
-      if (gs0) (void)hipStreamDestroy(gs0);
-      return fail(ctx, ALR_E_HIP, "rollout graph stream or events: %s", hipGetErrorString(e));
-    }
-    ctx->graph_stream = gs0;
-    ctx->graph_in = e0;
-    ctx->graph_out = e1;
-  }
-  hipStream_t gs = ctx->graph_stream;
+  hipStream_t gs = ctx->graph_stream;  // created by alr_set_rollout_graphs
   const std::array<uintptr_t, 12> key{
       (uintptr_t)n, (uintptr_t)block, (uintptr_t)ctx->h_dwork.size(), (uintptr_t)forced,
       (uintptr_t)feats_out, (uintptr_t)out.logprobs, (uintptr_t)out.tokens,
@@ -1644,6 +1628,22 @@ alr_status alr_set_rollout_graphs(alr_ctx* ctx, int32_t enable) {
   if (!ctx) return ALR_E_INVALID_ARG;
   if (enable != 0 && enable != 1)
     return fail(ctx, ALR_E_INVALID_ARG, "enable must be 0 or 1, got %d", enable);
+  if (enable == 1 && !ctx->graph_stream) {  // the stream and its two events: all three or none
+    hipStream_t gs0 = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&gs0, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&e0, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&e1, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      if (e1) (void)hipEventDestroy(e1);
+      if (e0) (void)hipEventDestroy(e0);
+      if (gs0) (void)hipStreamDestroy(gs0);
+      return fail(ctx, ALR_E_HIP, "rollout graph stream or events: %s", hipGetErrorString(e));
+    }
+    ctx->graph_stream = gs0;
+    ctx->graph_in = e0;
+    ctx->graph_out = e1;
+  }
   ctx->graphs_on = enable == 1;
   if (!ctx->graphs_on) drop_rollout_graphs(ctx);
   return ALR_OK;

@@ -138,6 +138,11 @@ def test_rollout_and_prefill_reject_null_context(lib):
     assert lib.alr_prefill(None, 1, binding._i32p(z), None, None, None, None, None) == 1
 
 
+def test_graph_switch_rejects_null_context(lib):
+    assert lib.alr_set_rollout_graphs(None, 1) == 1  # ALR_E_INVALID_ARG
+    assert lib.alr_set_rollout_graphs(None, 0) == 1
+
+
 def test_operands_of_4gib_are_rejected(lib):
     """The bf16 GEMM kernels address operand chunks by 32-bit byte offsets: a context whose
     activation operand (max(max_tokens, max_anchors) rows of max(d, F, H hd) bf16) or any weight
