@@ -44,7 +44,9 @@
  *
  * Memory and ownership.  All device memory is owned by the caller: weights,
  * inputs, outputs and one workspace whose size alr_workspace_bytes() gives.
- * The library allocates no device memory.  alr_create copies (repacks) the
+ * The library allocates no device memory (its code object holds the fixed
+ * scratch array of alr_rollout_topk_noalloc; opt-in rollout graphs hold the
+ * runtime's resources, see alr_set_rollout_graphs).  alr_create copies (repacks) the
  * weights into the workspace, so the weight buffers may be freed after it
  * returns.  The shared key/value cache lives in the workspace and stays valid
  * until the next alr_prefill on the same context.
