@@ -34,30 +34,43 @@ __global__ __launch_bounds__(256) void embed_kernel(float* __restrict__ resid,
   for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Elt<T>::ld(src + c);
 }
 
+// Four gain elements held in registers (fp32, or bf16 bit patterns)
+template <typename T>
+struct Gain4;
+template <>
+struct Gain4<float> {
+  f32x4 v;
+  __device__ __forceinline__ void load(const float* g) { v = *(const f32x4*)g; }
+  __device__ __forceinline__ float operator[](int e) const { return v[e]; }
+};
+template <>
+struct Gain4<bf16> {
+  u32x2 w;
+  __device__ __forceinline__ void load(const bf16* g) { w = *(const u32x2*)g; }
+  __device__ __forceinline__ float operator[](int e) const {
+    return bf2f((bf16)((e & 1) ? w[e >> 1] >> 16 : w[e >> 1] & 0xFFFFu));
+  }
+};
+
 // out[c .. c+3] = v * inv * g[c .. c+3], four elements at once
-__device__ __forceinline__ void norm4(float* o, f32x4 v, const float* g, float inv) {
-  const f32x4 gv = *(const f32x4*)g;
+__device__ __forceinline__ void norm4(float* o, f32x4 v, const Gain4<float>& g, float inv) {
   f32x4 w;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) w[e] = v[e] * inv * gv[e];
+  for (int e = 0; e < 4; ++e) w[e] = v[e] * inv * g[e];
   *(f32x4*)o = w;
 }
-__device__ __forceinline__ void norm4(bf16* o, f32x4 v, const bf16* g, float inv) {
-  const u32x2 gw = *(const u32x2*)g;
-  float gf[4];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    gf[2 * e] = bf2f((bf16)(gw[e] & 0xFFFFu));
-    gf[2 * e + 1] = bf2f((bf16)(gw[e] >> 16));
-  }
+__device__ __forceinline__ void norm4(bf16* o, f32x4 v, const Gain4<bf16>& g, float inv) {
   u32x2 w;
-  w[0] = pack2bf(v[0] * inv * gf[0], v[1] * inv * gf[1]);
-  w[1] = pack2bf(v[2] * inv * gf[2], v[3] * inv * gf[3]);
+  w[0] = pack2bf(v[0] * inv * g[0], v[1] * inv * g[1]);
+  w[1] = pack2bf(v[2] * inv * g[2], v[3] * inv * g[3]);
   *(u32x2*)o = w;
 }
 
 // out[r, :] = x[r, :] * g / sqrt(mean(x[r, :]^2) + eps); d a multiple of 4.  The
-// row stays in registers between the two passes for d <= 8192.
+// row and its gains stay in registers between the two passes for d <= 8192.
+// Every load of the row and of the gains is issued before the first use, so a
+// row costs one memory round trip instead of one per chunk (a load followed by
+// its use in the same conditional block makes the compiler wait there).
 template <typename T>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
                                                       const T* __restrict__ g,
@@ -68,14 +81,25 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   const float* xr = x + r * d;
   T* o = out + r * d;
   f32x4 v[CACHE];
-  float ss = 0.f;
+  Gain4<T> gv[CACHE];
 #pragma unroll
   for (int k = 0; k < CACHE; ++k) {
     const int c = (threadIdx.x + 256 * k) * 4;
     if (c < d) {
       v[k] = *(const f32x4*)(xr + c);
-      ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
+      gv[k].load(g + c);
     }
+  }
+  // vmcnt(0): the loads of every chunk have landed.  Without it the compiler
+  // cannot tell at the conditional stores below whether a gain load is still
+  // outstanding and waits before each store, and on this target such a wait
+  // also waits for the previous store.
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < CACHE; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
   }
   for (int c = (threadIdx.x + 256 * CACHE) * 4; c < d; c += 1024) {
     const f32x4 w = *(const f32x4*)(xr + c);
@@ -86,10 +110,13 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 #pragma unroll
   for (int k = 0; k < CACHE; ++k) {
     const int c = (threadIdx.x + 256 * k) * 4;
-    if (c < d) norm4(o + c, v[k], g + c, inv);
+    if (c < d) norm4(o + c, v[k], gv[k], inv);
   }
-  for (int c = (threadIdx.x + 256 * CACHE) * 4; c < d; c += 1024)
-    norm4(o + c, *(const f32x4*)(xr + c), g + c, inv);
+  for (int c = (threadIdx.x + 256 * CACHE) * 4; c < d; c += 1024) {
+    Gain4<T> gt;
+    gt.load(g + c);
+    norm4(o + c, *(const f32x4*)(xr + c), gt, inv);
+  }
 }
 
 // Row-major assembly from a table of source rows: dst row n = src[n] (K bf16
