@@ -379,8 +379,13 @@ struct has_set_split : std::false_type {};
 template <class Epi>
 struct has_set_split<Epi, decltype((void)&Epi::set_split)> : std::true_type {};
 
-// One thread per (row, column c in the low half of a 64-column group).
-template <class Epi>
+// One thread per (row, column c in the low half of a 64-column group).  With
+// S > 0 the slice count is S and every partial is loaded before the first add:
+// one memory round trip, where a load followed by its add in a loop over a
+// runtime count has the compiler wait in every iteration.  S = 0 reads
+// `slices` partials in such a loop.  Either way the slices are added in slice
+// order, so the result does not depend on S.
+template <class Epi, int S = 0>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part,
                                                             long sstride, int slices, int M,
                                                             int N, Epi epi) {
@@ -393,9 +398,23 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   const int col = g * 64 + c32;
   const float* p = part + (long)row * N + col;
   float lo = 0.f, hi = 0.f;
-  for (int sl = 0; sl < slices; ++sl) {
-    lo += p[sl * sstride];
-    hi += p[sl * sstride + 32];
+  if constexpr (S > 0) {
+    float a[S], b[S];
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+      a[sl] = p[sl * sstride];
+      b[sl] = p[sl * sstride + 32];
+    }
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+      lo += a[sl];
+      hi += b[sl];
+    }
+  } else {
+    for (int sl = 0; sl < slices; ++sl) {
+      lo += p[sl * sstride];
+      hi += p[sl * sstride + 32];
+    }
   }
   epi(row, col, lo, hi);
 }

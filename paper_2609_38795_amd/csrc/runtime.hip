@@ -415,6 +415,22 @@ struct ProfScope {
   }
 };
 
+// Sum of the S fp32 K-slice partials of an M x N product, then the real
+// epilogue; the slice counts the planner picks (2, 4) get kernels that load
+// every partial before the first add.
+template <class Epi>
+void launch_splitk_reduce(const float* part, long sstride, int S, int M, int N, const Epi& epi,
+                          hipStream_t st) {
+  const long thr = (long)M * (N / 64) * 32;
+  const unsigned nb = (unsigned)((thr + 255) / 256);
+  if (S == 2)
+    splitk_reduce_kernel<Epi, 2><<<nb, 256, 0, st>>>(part, sstride, S, M, N, epi);
+  else if (S == 4)
+    splitk_reduce_kernel<Epi, 4><<<nb, 256, 0, st>>>(part, sstride, S, M, N, epi);
+  else
+    splitk_reduce_kernel<Epi, 0><<<nb, 256, 0, st>>>(part, sstride, S, M, N, epi);
+}
+
 template <int TAG, typename T, class Epi>
 void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, int N, int K,
                  Epi epi, hipStream_t st, int force_tile = 0) {
@@ -462,9 +478,7 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         else
           gemm_bf16_kernel<TAG, 64, 128, 2, 2, 32, 4, EpiPartial>
               <<<t64 * S, 256, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
-        const long thr = (long)M * (N / 64) * 32;
-        splitk_reduce_kernel<Epi>
-            <<<(unsigned)((thr + 255) / 256), 256, 0, st>>>(ctx->splitk_buf, (long)M * N, S, M, N, epi);
+        launch_splitk_reduce(ctx->splitk_buf, (long)M * N, S, M, N, epi, st);
         return;
       }
       if (cfg == 20) cfg = 3;
@@ -482,9 +496,7 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         EpiPartial ep{ctx->splitk_buf, (long)M * N, N};
         gemm_bf16_pp64_kernel<TAG, EpiPartial>
             <<<t256 * S, 512, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
-        const long thr = (long)M * (N / 64) * 32;
-        splitk_reduce_kernel<Epi>
-            <<<(unsigned)((thr + 255) / 256), 256, 0, st>>>(ctx->splitk_buf, (long)M * N, S, M, N, epi);
+        launch_splitk_reduce(ctx->splitk_buf, (long)M * N, S, M, N, epi, st);
         return;
       }
       if (cfg == 18) cfg = 0;
