@@ -119,6 +119,63 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   }
 }
 
+// The reduce of a split-K residual update fused with the RMSNorm that reads the
+// updated residual, one workgroup per row of d <= 1024 CH elements:
+//   h[r, :] += part[0, r, :] + ... + part[S-1, r, :]
+// (the slices added in slice order and the sum then added to h, as
+// splitk_reduce_kernel with EpiResid does), the updated row copied to feature
+// row perm[r] (or r) when feat is set, and out[r, :] = RMSNorm(h[r, :]) * g with
+// the element order, sums and rounding of rmsnorm_kernel.  Every load of the
+// row (partials, residual, gains) is issued before the first add.
+template <typename T, int S, int CH>
+__global__ __launch_bounds__(256) void splitk_resid_norm_kernel(
+    const float* __restrict__ part, long sstride, float* __restrict__ h, float* __restrict__ feat,
+    long feat_rs, const int* __restrict__ perm, const T* __restrict__ g, T* __restrict__ out,
+    int d, float eps) {
+  __shared__ float red[4];
+  const long r = blockIdx.x;
+  float* hr = h + r * d;
+  const float* pr = part + r * d;
+  f32x4 v[CH], ps[CH][S];
+  Gain4<T> gv[CH];
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) {
+      v[k] = *(const f32x4*)(hr + c);
+#pragma unroll
+      for (int sl = 0; sl < S; ++sl) ps[k][sl] = *(const f32x4*)(pr + sl * sstride + c);
+      gv[k].load(g + c);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));  // vmcnt(0), as in rmsnorm_kernel
+  float* fr = feat ? feat + (perm ? (long)perm[r] : r) * feat_rs : nullptr;
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float acc = 0.f;
+#pragma unroll
+        for (int sl = 0; sl < S; ++sl) acc += ps[k][sl][e];
+        v[k][e] = v[k][e] + acc;
+      }
+      *(f32x4*)(hr + c) = v[k];
+      if (fr) *(f32x4*)(fr + c) = v[k];
+      ss += v[k][0] * v[k][0] + v[k][1] * v[k][1] + v[k][2] * v[k][2] + v[k][3] * v[k][3];
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const int c = (threadIdx.x + 256 * k) * 4;
+    if (c < d) norm4(out + r * d + c, v[k], gv[k], inv);
+  }
+}
+
 // Row-major assembly from a table of source rows: dst row n = src[n] (K bf16
 // elements, K a multiple of 8); used to build the fused weight matrices.
 __global__ __launch_bounds__(256) void gather_rows_ptr_kernel(bf16* __restrict__ dst,

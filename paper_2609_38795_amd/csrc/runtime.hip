@@ -431,9 +431,37 @@ void launch_splitk_reduce(const float* part, long sstride, int S, int M, int N, 
     splitk_reduce_kernel<Epi, 0><<<nb, 256, 0, st>>>(part, sstride, S, M, N, epi);
 }
 
+// The split-K reduce of a residual update together with the RMSNorm that reads
+// the updated rows (gains g, output out), when the row fits the fused kernel:
+// one launch instead of two, bit-identical to them.  false leaves both to the
+// caller.
+template <typename T>
+bool launch_splitk_resid_norm(alr_ctx* ctx, int S, int M, int N, const EpiResid& er, const T* g,
+                              T* out, hipStream_t st) {
+  if (er.ld != N || N % 4 != 0 || N > 8192 || (S != 2 && S != 4)) return false;
+  const int ch = (N + 1023) / 1024;
+  const float eps = ctx->cfg.rms_eps;
+  const float* part = ctx->splitk_buf;
+  const long ss = (long)M * N;
+#define ALR_RN(S_, CH_)                                                                     \
+  splitk_resid_norm_kernel<T, S_, CH_><<<M, 256, 0, st>>>(part, ss, er.h, er.feat, er.feat_rs, \
+                                                          er.perm, g, out, N, eps)
+  if (S == 2) {
+    if (ch <= 1) ALR_RN(2, 1); else if (ch <= 2) ALR_RN(2, 2); else if (ch <= 4) ALR_RN(2, 4); else ALR_RN(2, 8);
+  } else {
+    if (ch <= 1) ALR_RN(4, 1); else if (ch <= 2) ALR_RN(4, 2); else if (ch <= 4) ALR_RN(4, 4); else ALR_RN(4, 8);
+  }
+#undef ALR_RN
+  return true;
+}
+
+// norm_g / norm_out / normed: the RMSNorm that follows a residual update
+// (Epi = EpiResid).  When the product takes a split-K path, it is fused into
+// the reduce and *normed is set; otherwise the caller runs it.
 template <int TAG, typename T, class Epi>
 void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, int N, int K,
-                 Epi epi, hipStream_t st, int force_tile = 0) {
+                 Epi epi, hipStream_t st, int force_tile = 0, const T* norm_g = nullptr,
+                 T* norm_out = nullptr, bool* normed = nullptr) {
   if (M <= 0) return;
   ProfScope ps(ctx, TAG, st);
   if constexpr (std::is_same<T, bf16>::value) {
@@ -478,6 +506,12 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         else
           gemm_bf16_kernel<TAG, 64, 128, 2, 2, 32, 4, EpiPartial>
               <<<t64 * S, 256, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
+        if constexpr (std::is_same<Epi, EpiResid>::value) {
+          if (norm_out && normed && launch_splitk_resid_norm<T>(ctx, S, M, N, epi, norm_g, norm_out, st)) {
+            *normed = true;
+            return;
+          }
+        }
         launch_splitk_reduce(ctx->splitk_buf, (long)M * N, S, M, N, epi, st);
         return;
       }
@@ -496,6 +530,12 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
         EpiPartial ep{ctx->splitk_buf, (long)M * N, N};
         gemm_bf16_pp64_kernel<TAG, EpiPartial>
             <<<t256 * S, 512, 0, st>>>(A, lda, W, ldw, M, N, K / S, tm, tn, ep, S);
+        if constexpr (std::is_same<Epi, EpiResid>::value) {
+          if (norm_out && normed && launch_splitk_resid_norm<T>(ctx, S, M, N, epi, norm_g, norm_out, st)) {
+            *normed = true;
+            return;
+          }
+        }
         launch_splitk_reduce(ctx->splitk_buf, (long)M * N, S, M, N, epi, st);
         return;
       }
@@ -556,9 +596,15 @@ void rope_pair_rows(int n, int hd, std::vector<int>& dst_of_src) {
   }
 }
 
+// normed_in: the layer's input norm was already applied (fused into the
+// previous layer's down-projection reduce).  next_g / next_out: the RMSNorm
+// after this layer (the next layer's input norm or the final norm), which the
+// down projection fuses into its reduce when it takes a split-K path; then
+// *next_done is set.
 template <typename T>
 alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* feat,
-                         long feat_rs, const int* perm, hipStream_t st) {
+                         long feat_rs, const int* perm, bool normed_in, const T* next_g,
+                         T* next_out, bool* next_done, hipStream_t st) {
   const alr_config& c = ctx->cfg;
   const Layout& L = ctx->L;
   const int d = c.d_model, F = c.d_ffn, H = c.n_heads, G = c.n_kv_heads, hd = c.head_dim;
@@ -576,8 +622,9 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
   const int np = ctx->lim.max_block - 1;
   const long priv_rs = (long)np * kvd;
 
-  rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, reinterpret_cast<const T*>(lw + L.l_anorm), xn, d,
-                                       c.rms_eps);
+  if (!normed_in)
+    rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, reinterpret_cast<const T*>(lw + L.l_anorm), xn, d,
+                                         c.rms_eps);
   EpiQKV<T> eq;
   eq.q = qb;
   eq.cosT = ctx->at<float>(L.rope_cos);
@@ -677,14 +724,16 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
   er.feat = nullptr;
   er.feat_rs = 0;
   er.perm = nullptr;
+  const T* fnorm = reinterpret_cast<const T*>(lw + L.l_fnorm);
+  bool fnormed = false;
   if (decode)
     launch_gemm<ALR_PROF_DECODE_O, T>(ctx, at, qd, reinterpret_cast<const T*>(lw + L.l_o), qd, M,
-                                      d, qd, er, st);
+                                      d, qd, er, st, 0, fnorm, xn, &fnormed);
   else
     launch_gemm<ALR_PROF_PREFILL_O, T>(ctx, at, qd, reinterpret_cast<const T*>(lw + L.l_o), qd, M,
-                                       d, qd, er, st);
-  rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, reinterpret_cast<const T*>(lw + L.l_fnorm), xn, d,
-                                       c.rms_eps);
+                                       d, qd, er, st, 0, fnorm, xn, &fnormed);
+  if (!fnormed)
+    rmsnorm_kernel<T><<<M, 256, 0, st>>>(resid, fnorm, xn, d, c.rms_eps);
   EpiSwiGLU<T> es;
   es.out = act;
   es.ld = F;
@@ -697,12 +746,13 @@ alr_status layer_forward(alr_ctx* ctx, int l, int M, bool decode, int s, float* 
   er.feat = feat;
   er.feat_rs = feat_rs;
   er.perm = perm;
+  *next_done = false;
   if (decode)
     launch_gemm<ALR_PROF_DECODE_DOWN, T>(ctx, act, F, reinterpret_cast<const T*>(lw + L.l_down), F,
-                                         M, d, F, er, st);
+                                         M, d, F, er, st, 0, next_g, next_out, next_done);
   else
     launch_gemm<ALR_PROF_PREFILL_DOWN, T>(ctx, act, F, reinterpret_cast<const T*>(lw + L.l_down),
-                                          F, M, d, F, er, st);
+                                          F, M, d, F, er, st, 0, next_g, next_out, next_done);
   ALR_LAUNCHED(ctx, "mlp");
   return ALR_OK;
 }
@@ -735,14 +785,23 @@ alr_status prefill_impl(alr_ctx* ctx, int M, const int32_t* tokens, const void* 
       ALR_LAUNCHED(ctx, "transposed-V padding");
     }
   }
+  bool normed = false;  // the next layer's input norm (or the final norm) already applied
   for (int l = 0; l < c.n_layers; ++l) {
     const int f = feat_index(c, l);
     float* feat = f >= 0 ? ctx->at<float>(L.feat_store) + (long)f * d : nullptr;
-    const alr_status stt = layer_forward<T>(ctx, l, M, false, 0, feat, (long)nf * d, nullptr, st);
+    const bool last = l + 1 == c.n_layers;
+    const T* ng = last ? ctx->at<T>(L.w_fnorm)
+                       : reinterpret_cast<const T*>(ctx->layer(l + 1) + L.l_anorm);
+    T* no = last ? ctx->at<T>(L.hf_store) : ctx->at<T>(L.xnorm);
+    bool done = false;
+    const alr_status stt = layer_forward<T>(ctx, l, M, false, 0, feat, (long)nf * d, nullptr,
+                                            normed, ng, no, &done, st);
     if (stt != ALR_OK) return stt;
+    normed = done;
   }
-  rmsnorm_kernel<T><<<M, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
-                                       ctx->at<T>(L.hf_store), d, c.rms_eps);
+  if (!normed)
+    rmsnorm_kernel<T><<<M, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
+                                         ctx->at<T>(L.hf_store), d, c.rms_eps);
   ALR_LAUNCHED(ctx, "final norm");
   if (feats_out && nf > 0)
     ALR_HIP(ctx, hipMemcpyAsync(feats_out, ctx->at<float>(L.feat_store),
@@ -842,14 +901,22 @@ alr_status rollout_impl(alr_ctx* ctx, int n, int block, const int32_t* forced, c
     embed_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<int>(L.i_cur),
                                        ctx->at<T>(L.w_embed), nullptr, nullptr, d);
     ALR_LAUNCHED(ctx, "decode embed");
+    bool normed = false;  // as in the prefill
     for (int l = 0; l < c.n_layers; ++l) {
       const int f = feat_index(c, l);
       float* feat = (f >= 0 && feats_out) ? feats_out + ((long)s * nf + f) * d : nullptr;
-      stt = layer_forward<T>(ctx, l, n, true, s, feat, (long)block * nf * d, perm, st);
+      const T* ng = l + 1 == c.n_layers
+                        ? ctx->at<T>(L.w_fnorm)
+                        : reinterpret_cast<const T*>(ctx->layer(l + 1) + L.l_anorm);
+      bool done = false;
+      stt = layer_forward<T>(ctx, l, n, true, s, feat, (long)block * nf * d, perm, normed, ng,
+                             ctx->at<T>(L.xnorm), &done, st);
       if (stt != ALR_OK) return stt;
+      normed = done;
     }
-    rmsnorm_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
-                                         ctx->at<T>(L.xnorm), d, c.rms_eps);
+    if (!normed)
+      rmsnorm_kernel<T><<<n, 256, 0, st>>>(ctx->at<float>(L.resid), ctx->at<T>(L.w_fnorm),
+                                           ctx->at<T>(L.xnorm), d, c.rms_eps);
     stt = lm_head<T>(ctx, n, s, block, forced, out, true, nullptr, st);
     if (stt != ALR_OK) return stt;
   }
