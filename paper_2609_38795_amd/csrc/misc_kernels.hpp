@@ -20,18 +20,50 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return t;
 }
 
-// resid[r, :] = given[r, :] where mask[r] != 0, else E[tok[r], :]  (fp32 stream)
+// resid[r, :] = given[r, :] where mask[r] != 0, else E[tok[r], :]  (fp32 stream);
+// d a multiple of 16 / sizeof(T).  Each thread moves 16-byte chunks of the
+// source row, four at a time: the loads of a round are issued before its
+// stores, so a row costs a round trip per 4 x 256 chunks, not per element.
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(float* __restrict__ resid,
                                                     const int* __restrict__ tok,
                                                     const T* __restrict__ E,
                                                     const T* __restrict__ given,
                                                     const uint8_t* __restrict__ mask, int d) {
+  constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16-byte chunk
+  constexpr int U = 4;                      // chunks per thread per round
   const long r = blockIdx.x;
   const bool use_given = mask != nullptr && mask[r] != 0;
   const T* src = use_given ? given + r * d : E + (long)tok[r] * d;
   float* dst = resid + r * d;
-  for (int c = threadIdx.x; c < d; c += blockDim.x) dst[c] = Elt<T>::ld(src + c);
+  const int nch = d / EPC;
+  for (int c0 = threadIdx.x; c0 < nch; c0 += 256 * U) {
+    u32x4 w[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c0 + 256 * u < nch) w[u] = *(const u32x4*)(src + (long)(c0 + 256 * u) * EPC);
+    __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));  // vmcnt(0): the round's loads landed
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + 256 * u;
+      if (c >= nch) continue;
+      float* o = dst + (long)c * EPC;
+      if constexpr (sizeof(T) == 4) {
+        *(u32x4*)o = w[u];
+      } else {
+        f32x4 a, b;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          a[2 * e] = __uint_as_float(w[u][e] << 16);
+          a[2 * e + 1] = __uint_as_float(w[u][e] & 0xFFFF0000u);
+          b[2 * e] = __uint_as_float(w[u][2 + e] << 16);
+          b[2 * e + 1] = __uint_as_float(w[u][2 + e] & 0xFFFF0000u);
+        }
+        *(f32x4*)o = a;
+        *(f32x4*)(o + 4) = b;
+      }
+    }
+  }
 }
 
 // Four gain elements held in registers (fp32, or bf16 bit patterns)
