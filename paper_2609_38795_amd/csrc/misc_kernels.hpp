@@ -342,11 +342,21 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   }
   MaxArg acc = {-INFINITY, 0.f, 0x7FFFFFFF};
   const bool from_part = a.part != nullptr;
+  // Loads go out four at a time before their uses (one memory round trip per
+  // four, where a load used in the same iteration costs one each); every
+  // thread still visits its groups and columns in increasing order.
+  constexpr int U = 4;
   if (from_part) {
     const LogitPart* pr = a.part + (long)r * a.part_ld;
-    for (int g = threadIdx.x; g < a.part_ld; g += blockDim.x) {
-      const LogitPart q = pr[g];
-      acc = merge_maxarg(acc, MaxArg{q.m, q.s, 0x7FFFFFFF});
+    for (int g0 = threadIdx.x; g0 < a.part_ld; g0 += blockDim.x * U) {
+      LogitPart q[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (g0 + u * (int)blockDim.x < a.part_ld) q[u] = pr[g0 + u * blockDim.x];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (g0 + u * (int)blockDim.x < a.part_ld)
+          acc = merge_maxarg(acc, MaxArg{q[u].m, q[u].s, 0x7FFFFFFF});
     }
   } else {
     for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
@@ -412,8 +422,37 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   }
   float tsum = 0.f;  // exp(z - m) of the entries this thread dropped or never admitted
   int arg = 0x7FFFFFFF;  // this thread's first column equal to the row max
-  for (int c = threadIdx.x * 4; c < V; c += blockDim.x * 4) {
-    f32x4 v = *(const f32x4*)(z + c);
+  const int cstep = blockDim.x * 4;
+  if constexpr (!TOPK) {
+    // branch-free: the loads of a round are unconditional (a column past V
+    // re-reads the row's last chunk and is not used), the argmax is a select
+    for (int c0 = threadIdx.x * 4; c0 < V; c0 += cstep * U) {
+      f32x4 vv[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) vv[u] = *(const f32x4*)(z + min(c0 + u * cstep, V - 4));
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * cstep;
+        const bool in = c < V;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          arg = (in && arg == 0x7FFFFFFF && vv[u][e] == m) ? c + e : arg;  // columns rise
+          vv[u][e] -= lse;
+        }
+        if (in && a.write_lp) *(f32x4*)(z + c) = vv[u];
+      }
+    }
+  } else
+  for (int c0 = threadIdx.x * 4; c0 < V; c0 += cstep * U) {
+  f32x4 vv[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (c0 + u * cstep < V) vv[u] = *(const f32x4*)(z + c0 + u * cstep);
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int c = c0 + u * cstep;
+    if (c >= V) break;
+    f32x4 v = vv[u];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if (arg == 0x7FFFFFFF && v[e] == m) arg = c + e;  // columns rise within a thread
@@ -446,6 +485,7 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
       v[e] -= lse;
     }
     if (a.write_lp) *(f32x4*)(z + c) = v;
+  }
   }
   if (from_part) {  // lowest column holding the max over the block
 #pragma unroll
