@@ -424,8 +424,9 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
   int arg = 0x7FFFFFFF;  // this thread's first column equal to the row max
   const int cstep = blockDim.x * 4;
   if constexpr (!TOPK) {
-    // branch-free: the loads of a round are unconditional (a column past V
-    // re-reads the row's last chunk and is not used), the argmax is a select
+    // no data-dependent branch in the source: the loads of a round are
+    // unconditional (a column past V re-reads the row's last chunk, unused)
+    // and the argmax update is a select
     for (int c0 = threadIdx.x * 4; c0 < V; c0 += cstep * U) {
       f32x4 vv[U];
 #pragma unroll
@@ -442,50 +443,49 @@ __global__ __launch_bounds__(256) void lm_finalize_kernel(LmFinalize a) {
         if (in && a.write_lp) *(f32x4*)(z + c) = vv[u];
       }
     }
-  } else
-  for (int c0 = threadIdx.x * 4; c0 < V; c0 += cstep * U) {
-  f32x4 vv[U];
+  } else {
+    for (int c0 = threadIdx.x * 4; c0 < V; c0 += cstep * U) {
+      f32x4 vv[U];
 #pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (c0 + u * cstep < V) vv[u] = *(const f32x4*)(z + c0 + u * cstep);
+      for (int u = 0; u < U; ++u)
+        if (c0 + u * cstep < V) vv[u] = *(const f32x4*)(z + c0 + u * cstep);
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int c = c0 + u * cstep;
-    if (c >= V) break;
-    f32x4 v = vv[u];
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + u * cstep;
+        if (c >= V) break;
+        f32x4 v = vv[u];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (arg == 0x7FFFFFFF && v[e] == m) arg = c + e;  // columns rise within a thread
-      if constexpr (TOPK) {
-        // this thread meets ids in increasing order, so an equal value ranks
-        // after the entries already held: admit only strictly larger values
-        if (v[e] > tv[ALR_K_TOP - 1]) {
-          const float out_v = tv[ALR_K_TOP - 1];
-          if (out_v != -INFINITY) tsum += expf(out_v - m);
-          float pv = v[e];
-          int pi = c + e;
-          bool sh = false;
+        for (int e = 0; e < 4; ++e) {
+          if (arg == 0x7FFFFFFF && v[e] == m) arg = c + e;  // columns rise within a thread
+          // this thread meets ids in increasing order, so an equal value ranks
+          // after the entries already held: admit only strictly larger values
+          if (v[e] > tv[ALR_K_TOP - 1]) {
+            const float out_v = tv[ALR_K_TOP - 1];
+            if (out_v != -INFINITY) tsum += expf(out_v - m);
+            float pv = v[e];
+            int pi = c + e;
+            bool sh = false;
 #pragma unroll
-          for (int j = 0; j < ALR_K_TOP; ++j) {
-            const bool take = sh || (v[e] > tv[j]);
-            if (take) {
-              const float ov = tv[j];
-              const int oi = ti[j];
-              tv[j] = pv;
-              ti[j] = pi;
-              pv = ov;
-              pi = oi;
+            for (int j = 0; j < ALR_K_TOP; ++j) {
+              const bool take = sh || (v[e] > tv[j]);
+              if (take) {
+                const float ov = tv[j];
+                const int oi = ti[j];
+                tv[j] = pv;
+                ti[j] = pi;
+                pv = ov;
+                pi = oi;
+              }
+              sh = take;
             }
-            sh = take;
+          } else {
+            tsum += expf(v[e] - m);
           }
-        } else {
-          tsum += expf(v[e] - m);
+          v[e] -= lse;
         }
+        if (a.write_lp) *(f32x4*)(z + c) = v;
       }
-      v[e] -= lse;
     }
-    if (a.write_lp) *(f32x4*)(z + c) = v;
-  }
   }
   if (from_part) {  // lowest column holding the max over the block
 #pragma unroll
