@@ -103,10 +103,12 @@ def test_small_bf16_attention_paths(hd, H, G):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_wide_residual_rows(dtype):
     """d_model 8448: rows wider than the 8192 elements RMSNorm holds in registers, so every norm
-    also runs its streaming tail; the GEMMs see K = 8448 and 33 column tiles of 256."""
+    also runs its streaming tail; the GEMMs see K = 8448 and 33 column tiles of 256, and in bf16
+    the rollout's down projection (K = 1024) is split over K with rows too wide for the reduce fused
+    with the next norm, so the plain reduce and a separate norm run."""
     base = W.get("small_bf16")
     w = W.scaled(base, f"wide_{dtype}", n_layers=1, d_model=8448, n_heads=4, n_kv_heads=1,
-                 head_dim=64, d_ffn=256, vocab=512, feat_layers=(0,), dtype=dtype, n_seq=2,
+                 head_dim=64, d_ffn=1024, vocab=512, feat_layers=(0,), dtype=dtype, n_seq=2,
                  seq_len=96, anchors_per_seq=3, anchor_lo=0, anchor_hi=95, block=4)
     inp = W.Inputs(w, W.random_weights(w.shape, 8448, scale=0.02, norm_gain="random"),
                    W.random_tokens(512, (2, 96), 29, dist="zipf"),
