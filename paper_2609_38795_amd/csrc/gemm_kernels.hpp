@@ -33,6 +33,16 @@ __device__ __forceinline__ int vt_perm(int col) {
 // holds, in its low half, entries f = 32t .. 32t+31 of the list of
 // first-half dimensions (head = f / (hd/2), i = f % (hd/2)) and, in its high
 // half, their partners i + hd/2.  Outputs are written in natural order.
+// The rotation of a RoPE pair (lo, hi) by (cs, sn), with its single fused
+// multiply-add written out so that every epilogue form (per element, 16 rows,
+// 4 columns) rounds the same way whatever contraction the compiler would pick.
+__device__ __forceinline__ float rope_a(float lo, float hi, float cs, float sn) {
+  return fmaf(lo, cs, -(hi * sn));
+}
+__device__ __forceinline__ float rope_b(float lo, float hi, float cs, float sn) {
+  return fmaf(lo, sn, hi * cs);
+}
+
 template <typename OutT>
 struct EpiQKV {
   OutT* q;            // [M, H*hd]
@@ -65,8 +75,8 @@ struct EpiQKV {
       const int axis = (i < sec0) ? 0 : ((i < sec01) ? 1 : 2);
       const long p = (long)(pos[3 * row + axis] + pos_add);
       const float cs = cosT[p * half + i], sn = sinT[p * half + i];
-      Elt<OutT>::st(dst + head * hd + i, lo * cs - hi * sn);
-      Elt<OutT>::st(dst + head * hd + i + half, hi * cs + lo * sn);
+      Elt<OutT>::st(dst + head * hd + i, rope_a(lo, hi, cs, sn));
+      Elt<OutT>::st(dst + head * hd + i + half, rope_b(lo, hi, cs, sn));
     } else if (vt_col) {
       const long cl = c - qd - kd, col = vt_perm(vt_col[row]);
       Elt<OutT>::st(v + cl * vt_stride + col, lo);
@@ -76,6 +86,70 @@ struct EpiQKV {
       const int cl = c - qd - kd;
       Elt<OutT>::st(dst + cl, lo);
       Elt<OutT>::st(dst + cl + 32, hi);
+    }
+  }
+  // Columns c..c+3 and c+32..c+35 of one row (c a multiple of 4 in the low
+  // half of a 64-column group), for the split-K reduce: the same arithmetic
+  // per element as operator(), with 16-byte loads of the RoPE factors (the
+  // four dims share a head, and an axis unless an M-RoPE section boundary
+  // falls between them) and 8-byte bf16 stores.
+  __device__ __forceinline__ void quad(int row, int c, const f32x4& lo, const f32x4& hi) const {
+    const int half = hd >> 1;
+    const int qd = H * hd, kd = G * hd;
+    if (c < qd + kd) {
+      OutT* dst;
+      int cl;
+      if (c < qd) {
+        dst = q + (long)row * qd;
+        cl = c;
+      } else {
+        dst = k + (long)row * kv_rs;
+        cl = c - qd;
+      }
+      const int f = 32 * (cl >> 6) + (cl & 63);
+      const int head = f / half, i = f - head * half;
+      f32x4 cs, sn;
+      const int ax0 = (i < sec0) ? 0 : ((i < sec01) ? 1 : 2);
+      const int ax3 = (i + 3 < sec0) ? 0 : ((i + 3 < sec01) ? 1 : 2);
+      if (ax0 == ax3) {
+        const long o = (long)(pos[3 * row + ax0] + pos_add) * half + i;
+        cs = *(const f32x4*)(cosT + o);
+        sn = *(const f32x4*)(sinT + o);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int ie = i + e, ax = (ie < sec0) ? 0 : ((ie < sec01) ? 1 : 2);
+          const long o = (long)(pos[3 * row + ax] + pos_add) * half + ie;
+          cs[e] = cosT[o];
+          sn[e] = sinT[o];
+        }
+      }
+      f32x4 a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a[e] = rope_a(lo[e], hi[e], cs[e], sn[e]);
+        b[e] = rope_b(lo[e], hi[e], cs[e], sn[e]);
+      }
+      st4(dst + head * hd + i, a);
+      st4(dst + head * hd + i + half, b);
+    } else if (vt_col) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) (*this)(row, c + e, lo[e], hi[e]);
+    } else {
+      OutT* dst = v + (long)row * kv_rs;
+      const int cl = c - qd - kd;
+      st4(dst + cl, lo);
+      st4(dst + cl + 32, hi);
+    }
+  }
+  __device__ __forceinline__ static void st4(OutT* p, const f32x4& x) {
+    if constexpr (std::is_same<OutT, bf16>::value) {
+      u32x2 w;
+      w[0] = pack2bf(x[0], x[1]);
+      w[1] = pack2bf(x[2], x[3]);
+      *(u32x2*)p = w;
+    } else {
+      *(f32x4*)p = x;
     }
   }
   // The 16 rows of a lane's 32-row block (row of index t: rb + 8 (t >> 2) +
@@ -121,8 +195,8 @@ struct EpiQKV {
       for (int t = 0; t < 16; ++t)
         if (r[t] < M) {
           OutT* dst = base + (long)r[t] * rs + head * hd + i;
-          Elt<OutT>::st(dst, lo[t] * cs[t] - hi[t] * sn[t]);
-          Elt<OutT>::st(dst + half, hi[t] * cs[t] + lo[t] * sn[t]);
+          Elt<OutT>::st(dst, rope_a(lo[t], hi[t], cs[t], sn[t]));
+          Elt<OutT>::st(dst + half, rope_b(lo[t], hi[t], cs[t], sn[t]));
         }
     } else if (vt_col) {
       const long cl = c - qd - kd;
@@ -417,6 +491,47 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     }
   }
   epi(row, col, lo, hi);
+}
+
+template <class Epi, class = void>
+struct has_quad : std::false_type {};
+template <class Epi>
+struct has_quad<Epi, decltype((void)&Epi::quad)> : std::true_type {};
+
+// splitk_reduce_kernel for epilogues with quad(): one thread per (row, 4-column
+// run in the low half of a 64-column group) with 16-byte partial loads; each
+// element is summed in slice order as there.
+template <class Epi, int S>
+__global__ __launch_bounds__(256) void splitk_reduce4_kernel(const float* __restrict__ part,
+                                                             long sstride, int M, int N, Epi epi) {
+  const long t = (long)blockIdx.x * 256 + threadIdx.x;
+  const int groups = N / 64;
+  if (t >= (long)M * groups * 8) return;
+  const int c4 = (int)(t & 7);
+  const long rg = t >> 3;
+  const int g = (int)(rg % groups), row = (int)(rg / groups);
+  const int col = g * 64 + 4 * c4;
+  const float* p = part + (long)row * N + col;
+  f32x4 a[S], b[S];
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl) {
+    a[sl] = *(const f32x4*)(p + sl * sstride);
+    b[sl] = *(const f32x4*)(p + sl * sstride + 32);
+  }
+  f32x4 lo, hi;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    lo[e] = 0.f;
+    hi[e] = 0.f;
+  }
+#pragma unroll
+  for (int sl = 0; sl < S; ++sl)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[e] += a[sl][e];
+      hi[e] += b[sl][e];
+    }
+  epi.quad(row, col, lo, hi);
 }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM

@@ -421,6 +421,18 @@ struct ProfScope {
 template <class Epi>
 void launch_splitk_reduce(const float* part, long sstride, int S, int M, int N, const Epi& epi,
                           hipStream_t st) {
+  if constexpr (has_quad<Epi>::value) {
+    const long thr4 = (long)M * (N / 64) * 8;
+    const unsigned nb4 = (unsigned)((thr4 + 255) / 256);
+    if (S == 2) {
+      splitk_reduce4_kernel<Epi, 2><<<nb4, 256, 0, st>>>(part, sstride, M, N, epi);
+      return;
+    }
+    if (S == 4) {
+      splitk_reduce4_kernel<Epi, 4><<<nb4, 256, 0, st>>>(part, sstride, M, N, epi);
+      return;
+    }
+  }
   const long thr = (long)M * (N / 64) * 32;
   const unsigned nb = (unsigned)((thr + 255) / 256);
   if (S == 2)
