@@ -488,8 +488,10 @@ void launch_gemm(alr_ctx* ctx, const T* A, int lda, const T* W, int ldw, int M, 
     // Where 128x128 tiles alone give every CU the same number of tiles and
     // K <= 4096, writing and re-reading the fp32 partial sums costs more than
     // the ping-pong kernel gains (M = 1024, N = 4096: 46 vs 55 us), so those
-    // GEMMs take the 128x128 kernel with the epilogue fused.  With uneven
-    // rounds (N = 6144: 384 tiles on 256 CUs) split-K stays ahead.
+    // GEMMs take the 128x128 kernel with the epilogue fused (also where the
+    // split-K reduce would carry the following RMSNorm: 29.5 vs 26.3 + 2.9 ms
+    // per step for the rollout O projection).  With uneven rounds (N = 6144:
+    // 384 tiles on 256 CUs) split-K stays ahead.
     const bool fill128 = K <= 4096 && tiles(128, 128) % ctx->n_cu == 0;
     // the output head's per-group partials are formed in the epilogue of each
     // tile; a split-K reduce hands it columns in another arrangement
