@@ -16,10 +16,11 @@ def _print(*a):
     print(*a, flush=True)
 
 
-def _mrope_inputs(dtype, hd, H, G, sections, side, seed):
+def _mrope_inputs(dtype, hd, H, G, sections, side, seed, d_model=256):
     base = W.get("tiny_fp32")
     L = 160
-    w = W.scaled(base, f"mrope_{dtype}_{hd}", n_layers=2, d_model=256, n_heads=H, n_kv_heads=G,
+    w = W.scaled(base, f"mrope_{dtype}_{hd}_{d_model}", n_layers=2, d_model=d_model, n_heads=H,
+                 n_kv_heads=G,
                  head_dim=hd, d_ffn=512, vocab=1024, feat_layers=(0, 1), dtype=dtype,
                  mrope_sections=sections, n_seq=2, seq_len=L, anchors_per_seq=6,
                  anchor_lo=side * side, anchor_hi=L - 1, block=6)
@@ -51,11 +52,15 @@ def _prefill(eng, inp, pos):
     eng.prefill(toks, [w.seq_len] * w.n_seq, emb, mask, positions=pos.reshape(-1, 3))
 
 
-@pytest.mark.parametrize("dtype,hd,H,G,sections", [("f32", 32, 4, 2, (4, 6, 6)),
-                                                   ("bf16", 128, 4, 2, (16, 24, 24)),
-                                                   ("bf16", 64, 8, 2, (8, 12, 12))])
-def test_mrope_rollout_matches_oracle(dtype, hd, H, G, sections):
-    inp, pos = _mrope_inputs(dtype, hd, H, G, sections, side=6, seed=hd + H)
+# the last case puts section boundaries (6 and 19) inside runs of four rotary dims and is wide
+# enough (d_model 512) for the rollout's QKV product to be split over K, so the split-K reduce's
+# four-column RoPE meets both a shared axis and the per-dim fallback
+@pytest.mark.parametrize("dtype,hd,H,G,sections,d_model", [("f32", 32, 4, 2, (4, 6, 6), 256),
+                                                           ("bf16", 128, 4, 2, (16, 24, 24), 256),
+                                                           ("bf16", 64, 8, 2, (8, 12, 12), 256),
+                                                           ("bf16", 64, 8, 2, (6, 13, 13), 512)])
+def test_mrope_rollout_matches_oracle(dtype, hd, H, G, sections, d_model):
+    inp, pos = _mrope_inputs(dtype, hd, H, G, sections, side=6, seed=hd + H, d_model=d_model)
     w = inp.workload
     eng = make_engine(inp)
     _prefill(eng, inp, pos)
