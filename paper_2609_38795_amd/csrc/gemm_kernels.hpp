@@ -312,12 +312,43 @@ template <typename OutT>
 struct EpiSwiGLU {
   OutT* out;
   int ld;
+  // SiLU(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
+  // 2 ulp of fp32; e^-g overflowing to inf gives the limit 0), times u
+  __device__ static __forceinline__ float act(float g, float u) {
+    const float s = g * __builtin_amdgcn_rcpf(1.0f + fast_exp2(-1.44269504088896341f * g));
+    return s * u;
+  }
   __device__ __forceinline__ void operator()(int row, int c, float g, float u) const {
     const int col = (c >> 6) * 32 + (c & 63);
-    // SiLU(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
-    // 2 ulp of fp32; e^-g overflowing to inf gives the limit 0)
-    const float s = g * __builtin_amdgcn_rcpf(1.0f + fast_exp2(-1.44269504088896341f * g));
-    Elt<OutT>::st(out + (long)row * ld + col, s * u);
+    Elt<OutT>::st(out + (long)row * ld + col, act(g, u));
+  }
+  // Rows rb + 8 q + e of one column: the even and odd lanes of a pair trade
+  // one value per two rows (DPP quad swap), so the even lane writes row r at
+  // columns col, col+1 and the odd lane row r+1 at col-1, col — one store of
+  // two elements in place of two single-element stores.  Needs the pair's
+  // output columns to start at an even column (d_ffn is a multiple of 64).
+  __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
+                                         const float* hi) const {
+    const int odd = c & 1;
+    const int col = (c >> 6) * 32 + (c & 63) - odd;
+    float y[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) y[t] = act(lo[t], hi[t]);
+#pragma unroll
+    for (int t = 0; t < 16; t += 2) {
+      const float x = dpp_perm<0xB1>(odd ? y[t] : y[t + 1]);
+      const float a = odd ? x : y[t], b = odd ? y[t + 1] : x;
+      const int r = rb + 8 * (t >> 2) + (t & 3) + odd;
+      if (r < M) st2(out + (long)r * ld + col, a, b);
+    }
+  }
+  __device__ static __forceinline__ void st2(float* p, float a, float b) {
+    *reinterpret_cast<float2*>(p) = make_float2(a, b);
+  }
+  __device__ static __forceinline__ void st2(bf16* p, float a, float b) {
+    const unsigned lo = __builtin_bit_cast(unsigned short, f2bf(a));
+    const unsigned hi = __builtin_bit_cast(unsigned short, f2bf(b));
+    *reinterpret_cast<unsigned*>(p) = lo | (hi << 16);
   }
 };
 
