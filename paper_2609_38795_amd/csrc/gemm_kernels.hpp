@@ -43,6 +43,16 @@ __device__ __forceinline__ float rope_b(float lo, float hi, float cs, float sn) 
   return fmaf(lo, sn, hi * cs);
 }
 
+// Lanes 2j and 2j+1 of an MFMA accumulator hold adjacent columns c, c+1 (c
+// even) of the same rows.  Given a lane's values x_r, x_r1 of rows r and r+1,
+// one DPP quad swap leaves the even lane with row r at columns c, c+1 and the
+// odd lane with row r+1 at columns c, c+1, so each lane writes (or reads) two
+// adjacent elements with one access instead of two.
+__device__ __forceinline__ f32x2 pair_rows(int odd, float x_r, float x_r1) {
+  const float x = dpp_perm<0xB1>(odd ? x_r : x_r1);
+  return odd ? f32x2{x, x_r1} : f32x2{x_r, x};
+}
+
 template <typename OutT>
 struct EpiQKV {
   OutT* q;            // [M, H*hd]
@@ -142,6 +152,12 @@ struct EpiQKV {
       st4(dst + cl + 32, hi);
     }
   }
+  __device__ __forceinline__ static void st2(OutT* p, const f32x2& x) {
+    if constexpr (std::is_same<OutT, bf16>::value)
+      *(uint32_t*)p = pack2bf(x[0], x[1]);
+    else
+      *(f32x2*)p = x;
+  }
   __device__ __forceinline__ static void st4(OutT* p, const f32x4& x) {
     if constexpr (std::is_same<OutT, bf16>::value) {
       u32x2 w;
@@ -191,13 +207,27 @@ struct EpiQKV {
         cs[t] = cosT[o];
         sn[t] = sinT[o];
       }
+      // The two lanes of a column pair (i even, i+1 in the same head since half
+      // is even) trade one value of each half per two rows, so the even lane
+      // writes row r at i, i+1 and the odd lane row r+1: one store of two
+      // elements per half instead of two single-element stores.
+      const int odd = c & 1;
+      float a[16], b[16];
 #pragma unroll
-      for (int t = 0; t < 16; ++t)
-        if (r[t] < M) {
-          OutT* dst = base + (long)r[t] * rs + head * hd + i;
-          Elt<OutT>::st(dst, rope_a(lo[t], hi[t], cs[t], sn[t]));
-          Elt<OutT>::st(dst + half, rope_b(lo[t], hi[t], cs[t], sn[t]));
+      for (int t = 0; t < 16; ++t) {
+        a[t] = rope_a(lo[t], hi[t], cs[t], sn[t]);
+        b[t] = rope_b(lo[t], hi[t], cs[t], sn[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < 16; t += 2) {
+        const f32x2 pa = pair_rows(odd, a[t], a[t + 1]), pb = pair_rows(odd, b[t], b[t + 1]);
+        const int rr = r[t] + odd;
+        if (rr < M) {
+          OutT* dst = base + (long)rr * rs + head * hd + i - odd;
+          st2(dst, pa);
+          st2(dst + half, pb);
         }
+      }
     } else if (vt_col) {
       const long cl = c - qd - kd;
       int col[16];
@@ -239,10 +269,11 @@ struct EpiQKV {
   }
 };
 
-// Epilogues that read memory define rows16(): a lane's 16 rows of a 32-row
-// block at once, all loads before all stores (the compiler cannot prove that a
-// later row's load does not alias an earlier row's store, so element-wise
-// calls would wait for one load round trip per row).
+// Epilogues that read memory, or that write two columns per access, define
+// rows16(): a lane's 16 rows of a 32-row block at once, all loads before all
+// stores (the compiler cannot prove that a later row's load does not alias an
+// earlier row's store, so element-wise calls would wait for one load round
+// trip per row).
 template <class Epi, class = void>
 struct has_rows16 : std::false_type {};
 template <class Epi>
@@ -322,11 +353,9 @@ struct EpiSwiGLU {
     const int col = (c >> 6) * 32 + (c & 63);
     Elt<OutT>::st(out + (long)row * ld + col, act(g, u));
   }
-  // Rows rb + 8 q + e of one column: the even and odd lanes of a pair trade
-  // one value per two rows (DPP quad swap), so the even lane writes row r at
-  // columns col, col+1 and the odd lane row r+1 at col-1, col — one store of
-  // two elements in place of two single-element stores.  Needs the pair's
-  // output columns to start at an even column (d_ffn is a multiple of 64).
+  // Rows rb + 8 q + e of one column, written two columns per store after the
+  // lane-pair exchange (pair_rows); the pair's first output column is even
+  // because d_ffn is a multiple of 64.
   __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
                                          const float* hi) const {
     const int odd = c & 1;
@@ -336,19 +365,15 @@ struct EpiSwiGLU {
     for (int t = 0; t < 16; ++t) y[t] = act(lo[t], hi[t]);
 #pragma unroll
     for (int t = 0; t < 16; t += 2) {
-      const float x = dpp_perm<0xB1>(odd ? y[t] : y[t + 1]);
-      const float a = odd ? x : y[t], b = odd ? y[t + 1] : x;
+      const f32x2 x = pair_rows(odd, y[t], y[t + 1]);
       const int r = rb + 8 * (t >> 2) + (t & 3) + odd;
-      if (r < M) st2(out + (long)r * ld + col, a, b);
+      if (r < M) {
+        if constexpr (std::is_same<OutT, bf16>::value)
+          *(uint32_t*)(out + (long)r * ld + col) = pack2bf(x[0], x[1]);
+        else
+          *(f32x2*)(out + (long)r * ld + col) = x;
+      }
     }
-  }
-  __device__ static __forceinline__ void st2(float* p, float a, float b) {
-    *reinterpret_cast<float2*>(p) = make_float2(a, b);
-  }
-  __device__ static __forceinline__ void st2(bf16* p, float a, float b) {
-    const unsigned lo = __builtin_bit_cast(unsigned short, f2bf(a));
-    const unsigned hi = __builtin_bit_cast(unsigned short, f2bf(b));
-    *reinterpret_cast<unsigned*>(p) = lo | (hi << 16);
   }
 };
 
