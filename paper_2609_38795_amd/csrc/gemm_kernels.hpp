@@ -299,10 +299,34 @@ struct EpiResid {
       f[32] = b;
     }
   }
-  // In two halves of 8 rows (loads, then stores), which bounds the registers
-  // the epilogue needs inside a persistent kernel.
+  // Without feature rows all 16 rows' loads are issued before the first store,
+  // so a wave waits one memory round trip per 32-row block instead of one per
+  // 8 rows (the whole workgroup reaches its epilogue together, and those waits
+  // leave the CU's matrix cores idle).  With feature rows (and their
+  // permutation indices) two halves of 8 rows bound the registers the
+  // epilogue needs inside a persistent kernel.
   __device__ __forceinline__ void rows16(int rb, int M, int c, const float* lo,
                                          const float* hi) const {
+    if (!feat) {
+      float a[16], b[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const int rc = min(rb + 8 * (t >> 2) + (t & 3), M - 1);
+        const float* p = h + (long)rc * ld + c;
+        a[t] = p[0];
+        b[t] = p[32];
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const int r = rb + 8 * (t >> 2) + (t & 3);
+        if (r < M) {
+          float* p = h + (long)r * ld + c;
+          p[0] = a[t] + lo[t];
+          p[32] = b[t] + hi[t];
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
       int fr[8];
@@ -314,7 +338,7 @@ struct EpiResid {
         const float* p = h + (long)rc * ld + c;
         a[u] = p[0];
         b[u] = p[32];
-        fr[u] = (feat && perm) ? perm[rc] : r;
+        fr[u] = perm ? perm[rc] : r;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -326,11 +350,9 @@ struct EpiResid {
           float* p = h + (long)r * ld + c;
           p[0] = a[u];
           p[32] = b[u];
-          if (feat) {
-            float* f = feat + (long)fr[u] * feat_rs + c;
-            f[0] = a[u];
-            f[32] = b[u];
-          }
+          float* f = feat + (long)fr[u] * feat_rs + c;
+          f[0] = a[u];
+          f[32] = b[u];
         }
       }
     }
