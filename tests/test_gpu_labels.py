@@ -161,7 +161,7 @@ def test_corpus_labels_match_oracle_tiny():
 
 
 def test_corpus_slot0_equals_rollout_slot0_bit_exact():
-    """Slot 1 gets identical supervision under KD and ALR: the same GPU rows."""
+    """At slot 1 the KD labels and the ALR labels coincide: both come from the same GPU rows."""
     inp = _small_bf16_inputs()
     w = inp.workload
     eng = make_engine(inp)
