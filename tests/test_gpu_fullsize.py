@@ -33,6 +33,7 @@ to the sampled anchors, so it stays in the same launch configuration.
 """
 import dataclasses
 import os
+import sys
 import time
 
 import numpy as np
@@ -51,7 +52,8 @@ torch = pytest.importorskip("torch")
 
 
 def _log(msg):
-    print(f"[fullsize] {msg}", flush=True)
+    # the real stderr, past pytest's capture: a full-size case runs for minutes
+    print(f"[fullsize] {msg}", file=sys.__stderr__, flush=True)
 
 
 _INPUTS = {}
