@@ -33,7 +33,6 @@ to the sampled anchors, so it stays in the same launch configuration.
 """
 import dataclasses
 import os
-import sys
 import time
 
 import numpy as np
@@ -51,9 +50,26 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1200)]
 torch = pytest.importorskip("torch")
 
 
+_CAPMAN = None
+
+
+@pytest.fixture(autouse=True)
+def _capture_manager(request):
+    global _CAPMAN
+    _CAPMAN = request.config.pluginmanager.getplugin("capturemanager")
+    yield
+    _CAPMAN = None
+
+
 def _log(msg):
-    # the real stderr, past pytest's capture: a full-size case runs for minutes
-    print(f"[fullsize] {msg}", file=sys.__stderr__, flush=True)
+    # a full-size case runs for minutes: its progress lines go out as they
+    # happen, with pytest's output capture suspended for the write
+    line = f"[fullsize] {msg}"
+    if _CAPMAN is None:
+        print(line, flush=True)
+        return
+    with _CAPMAN.global_and_fixture_disabled():
+        print(line, flush=True)
 
 
 _INPUTS = {}
